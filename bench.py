@@ -1,0 +1,208 @@
+"""Benchmark: tiled exact attention on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+    python bench.py --config NAME      # one workload only (own JSON line)
+
+A step is one pass of the whole hot path over one batch of synthetic input:
+prefill attention on B=4 H=16 Sq=Skv=2048 d=128 causal (attn_fwd), then
+Flash-Decode on B=16 H=32 Skv=8192 d=128 (attn_decode: split partials +
+combine).  Inputs are seeded bf16 N(0,1) tensors resident in HBM before the
+timed region.  Each kernel call is bracketed by HIP events on the stream it
+runs on; the step wall time is bracketed by device synchronisation.
+
+Printed (one JSON line): value = prefill TFLOP/s (algorithmic flops: 4*d per
+unmasked (query, key) pair) with its MFMA roofline fraction; the decode leg's
+HBM GB/s (algorithmic bytes: K, V, Q read once, O written once) with its HBM
+roofline fraction; and the fp64 CPU oracle's rate on a bounded sample of the
+prefill workload, timed on this host's cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6  # 256 CU x 4096 flop/clk x 2.4 GHz (dense bf16 MFMA)
+PEAK_HBM_GBS = 8000.0      # HBM3E
+
+
+def _args():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="target CPU time for the oracle sample")
+    ap.add_argument("--config", default=None, help="bench a single named workload")
+    return ap.parse_args()
+
+
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor()
+
+
+def _time_calls(fn, steps: int, warmup: int):
+    """Per-call device time (ms) from HIP events on the current stream."""
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    t0 = time.perf_counter()
+    for a, b in evs:
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps * 1e3
+    ms = sorted(a.elapsed_time(b) for a, b in evs)
+    return sum(ms) / len(ms), ms[len(ms) // 2], wall
+
+
+def _load_workload(w, dev):
+    from attn_inputs import make_inputs
+    q, k, v = make_inputs(w)
+    return q, k, v, q.to(dev), k.to(dev), v.to(dev)
+
+
+def cpu_baseline(w, q, k, v, target_s: float) -> dict:
+    """The fp64 oracle on whole (b, h) slabs of the prefill workload."""
+    import oracle
+    import numpy as np
+    heads = w.B * w.H
+    qs, ks, vs = (t.reshape(heads, 1, t.shape[2], w.d) for t in (q, k, v))
+
+    def run(n):
+        t0 = time.perf_counter()
+        oracle.attn(qs[:n].contiguous(), ks[:n].contiguous(), vs[:n].contiguous(), n, 1, w.Sq,
+                    w.Skv, w.d, w.scale, w.causal)
+        return time.perf_counter() - t0
+
+    t1 = run(1)
+    n = int(max(1, min(heads, target_s / max(t1, 1e-6))))
+    t = run(n) if n > 1 else t1
+    sample = w.with_(B=1, H=n)
+    flops = sample.flops()
+    return {"value": flops / t / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"{n} of {heads} (b,h) slabs of {w.name} ({flops / 1e9:.2f} GFLOP in "
+                      f"{t:.2f} s, fp64, {_cpu_model()})",
+            "seconds": t}
+
+
+def main():
+    a = _args()
+    if a.gpus != 1:
+        print(f"bench.py runs on exactly one GPU (asked for {a.gpus}); the path has no "
+              "multi-GPU form in this build", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2609_29219_amd as pa
+    from attn_inputs import BY_NAME, CONFIGS
+
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    if a.config:
+        w = BY_NAME[a.config]
+        q, k, v, qd, kd, vd = _load_workload(w, dev)
+        if w.kind == "fwd":
+            o = torch.empty((w.B, w.H, w.Sq, w.d), dtype=torch.float32, device=dev)
+            fn = lambda: pa.attn_fwd(qd, kd, vd, o=o, scale=w.scale, causal=w.causal)  # noqa: E731
+            plan = pa.get_plan(pa.KIND_FWD, w.B, w.H, w.Sq, w.Skv, w.d, w.causal)
+        else:
+            o = torch.empty((w.B, w.H, w.d), dtype=torch.float32, device=dev)
+            fn = lambda: pa.attn_decode(qd, kd, vd, o=o)  # noqa: E731
+            plan = pa.get_plan(pa.KIND_DECODE, w.B, w.H, 1, w.Skv, w.d)
+        mean_ms, med_ms, wall = _time_calls(fn, a.steps, a.warmup)
+        rec = {"workload": w.name, "ms_mean": mean_ms, "ms_median": med_ms,
+               "ms_wall_per_call": wall, "plan": plan}
+        if w.kind == "fwd":
+            rec["tflops"] = w.flops() / (mean_ms * 1e-3) / 1e12
+            rec["frac_mfma_peak"] = rec["tflops"] / PEAK_BF16_TFLOPS
+        rec["gbs"] = w.hbm_bytes() / (mean_ms * 1e-3) / 1e9
+        rec["frac_hbm_peak"] = rec["gbs"] / PEAK_HBM_GBS
+        print(json.dumps(rec), flush=True)
+        return
+
+    wp, wd = CONFIGS[1], CONFIGS[3]
+    qp, kp, vp, qpd, kpd, vpd = _load_workload(wp, dev)
+    _, _, _, qdd, kdd, vdd = _load_workload(wd, dev)
+    op = torch.empty((wp.B, wp.H, wp.Sq, wp.d), dtype=torch.float32, device=dev)
+    od = torch.empty((wd.B, wd.H, wd.d), dtype=torch.float32, device=dev)
+
+    def fwd():
+        pa.attn_fwd(qpd, kpd, vpd, o=op, scale=wp.scale, causal=wp.causal)
+
+    def dec():
+        pa.attn_decode(qdd, kdd, vdd, o=od)
+
+    for _ in range(a.warmup):
+        fwd()
+        dec()
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(a.steps)]
+    t0 = time.perf_counter()
+    for e0, e1, e2 in ev:
+        e0.record()
+        fwd()
+        e1.record()
+        dec()
+        e2.record()
+    torch.cuda.synchronize()
+    ms_per_step = (time.perf_counter() - t0) / a.steps * 1e3
+    fwd_ms = sum(e0.elapsed_time(e1) for e0, e1, _ in ev) / a.steps
+    dec_ms = sum(e1.elapsed_time(e2) for _, e1, e2 in ev) / a.steps
+
+    tflops = wp.flops() / (fwd_ms * 1e-3) / 1e12
+    gbs = wd.hbm_bytes() / (dec_ms * 1e-3) / 1e9
+    fplan = pa.get_plan(pa.KIND_FWD, wp.B, wp.H, wp.Sq, wp.Skv, wp.d, wp.causal)
+    dplan = pa.get_plan(pa.KIND_DECODE, wd.B, wd.H, 1, wd.Skv, wd.d)
+    rec = {
+        "metric": "Attention TFLOP/s + % MFMA peak (prefill); KV HBM GB/s + % peak (decode)",
+        "value": tflops,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded bf16 N(0,1), resident in HBM)",
+        "config": {"workload": f"{wp.name} + {wd.name}",
+                   "prefill": {"B": wp.B, "H": wp.H, "Sq": wp.Sq, "Skv": wp.Skv, "d": wp.d,
+                               "causal": wp.causal, "plan": fplan},
+                   "decode": {"B": wd.B, "H": wd.H, "Skv": wd.Skv, "d": wd.d, "plan": dplan}},
+        "roofline": {"bound": "mfma", "achieved": tflops, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": tflops / PEAK_BF16_TFLOPS, "traffic": None,
+                     "kernel": "fwd_kernel", "ms_per_launch": fwd_ms,
+                     "flops_per_launch": wp.flops()},
+        "decode": {"value": gbs, "unit": "GB/s", "ms_per_call": dec_ms,
+                   "roofline": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS,
+                                "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS, "traffic": None,
+                                "kernel": "decode_partial_kernel + decode_combine_kernel",
+                                "bytes_per_call": wd.hbm_bytes()}},
+    }
+    if not a.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(wp, qp, kp, vp, a.cpu_seconds)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,141 @@
+/*
+ * attn.h -- C ABI of libattn.so: tiled exact softmax attention on MI355X
+ * (gfx950), prefill (FlashAttention forward) and split-KV Flash-Decode.
+ *
+ * The operation.  The paper evaluates two attention kernels (Evaluation,
+ * "Experimental Setup" and the Flash Attention / Flash Decode paragraphs):
+ * Flash Attention, which combines a matrix multiplication, a softmax and a
+ * value aggregation, and Flash Decode, where the query length is one and
+ * the sequence (reduction) axis is split across cores, followed by a gather
+ * of partial results, a global softmax and the final output (HEG paragraph
+ * of the latency-modelling section).  Written out, for every batch b, head h
+ * and query row i:
+ *     s_ij   = scale * sum_c q[b][h][i][c] * k[b][h][j][c]
+ *     o[b][h][i][c] = sum_{j in A_i} exp(s_ij) v[b][h][j][c] / sum_{j in A_i} exp(s_ij)
+ * with A_i = {0..Skv-1} (non-causal) or {j : j <= i + Skv - Sq} (causal,
+ * aligned to the bottom-right corner of the score matrix).
+ *
+ * Conventions common to every call:
+ *   - q, k, v, o are DEVICE pointers (e.g. torch.Tensor.data_ptr() of a
+ *     CUDA/HIP tensor), contiguous, 16-byte aligned.  The caller owns them
+ *     and keeps them alive until the stream has executed the work.
+ *   - bf16 means IEEE bfloat16 bit patterns (uint16 storage).
+ *   - All calls are asynchronous on the stream set by attn_set_stream()
+ *     (per host thread; the default is the null stream).  They return after
+ *     enqueueing and never synchronise; device faults surface at the
+ *     caller's next synchronisation.
+ *   - Arguments are validated on the host before anything is launched; on
+ *     error nothing is launched and o is untouched.
+ *   - Return codes: ATTN_OK (0) or a negative ATTN_E* code; the message of
+ *     the last failing call on this host thread is in attn_last_error().
+ *   - There is no CPU fallback: without a gfx950 device the compute calls
+ *     return ATTN_EUNSUPPORTED or ATTN_EHIP.
+ */
+#ifndef ATTN_H
+#define ATTN_H
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ATTN_OK 0
+#define ATTN_EINVAL (-1)       /* null or misaligned pointer, a dim <= 0, bad buffer length */
+#define ATTN_EUNSUPPORTED (-2) /* d not in {64,128}, causal with Sq > Skv, device not gfx950 */
+#define ATTN_EHIP (-3)         /* HIP runtime or launch error (message in attn_last_error) */
+#define ATTN_ENOMEM (-4)       /* decode workspace allocation failed */
+
+#define ATTN_KIND_FWD 0
+#define ATTN_KIND_DECODE 1
+
+/*
+ * Prefill attention (Flash Attention).
+ *   q: bf16 [B][H][Sq][d]      k, v: bf16 [B][H][Skv][d]
+ *   o: fp32 [B][H][Sq][d]      (caller-allocated, fully overwritten)
+ *   scale: softmax scale applied to q.k (typically 1/sqrt(d)).
+ *   causal: 0 = every key, 1 = key j allowed for row i iff j <= i + Skv - Sq.
+ * Supported: d in {64, 128}; any B, H, Sq, Skv >= 1 (ragged tails are
+ * handled); causal requires Sq <= Skv.  B*H*Sq*d and B*H*Skv*d must fit in
+ * int64.  Work: QK^T and PV on bf16 MFMA with fp32 accumulation, online
+ * softmax in fp32; the probabilities are rounded to bf16 before PV and the
+ * normaliser sums the rounded values.
+ */
+int attn_fwd(const void* q, const void* k, const void* v, float* o, int B, int H, int Sq,
+             int Skv, int d, float scale, int causal);
+
+/*
+ * Single-query attention with the KV sequence split across workgroups
+ * (Flash Decode), then a log-sum-exp combine of the partial results.
+ *   q: bf16 [B][H][d]      k, v: bf16 [B][H][Skv][d]      o: fp32 [B][H][d]
+ *   scale is fixed to (float)(1/sqrt(d)).
+ *   n_splits <= 0: the planner chooses the split count from the device's
+ *   compute-unit count and HBM model; otherwise it is clamped to [1, Skv]
+ *   and the chunk is ceil(Skv / n_splits) keys (empty splits are never
+ *   launched).  Every split count gives the same result up to fp32
+ *   rounding.
+ * Workspace: the library allocates B*H*n*(d+2)*4 bytes stream-ordered from
+ * its own memory pool and frees it stream-ordered after the combine; it
+ * returns ATTN_ENOMEM if that allocation fails.
+ */
+int attn_decode(const void* q, const void* k, const void* v, float* o, int B, int H, int Skv,
+                int d, int n_splits);
+
+/* Set the HIP stream (hipStream_t, or NULL for the null stream) used by
+ * this host thread's subsequent calls.  Returns ATTN_OK. */
+int attn_set_stream(void* hip_stream);
+
+/* The stream currently set for this host thread. */
+void* attn_get_stream(void);
+
+/* Message describing the last failing call on this host thread ("" if none).
+ * The pointer stays valid until the next call on this thread. */
+const char* attn_last_error(void);
+
+/*
+ * Architecture description used by the planner (cf. the paper's
+ * architecture-description section: structural properties from the
+ * specification, performance properties from microbenchmarks).
+ */
+typedef struct attn_device_desc {
+    char arch[32];              /* e.g. "gfx950" */
+    int num_cus;                /* compute units */
+    int num_xcds;               /* accelerator complex dies (separate L2s) */
+    int simds_per_cu;           /* 4 on CDNA */
+    int wave_size;              /* 64 */
+    int lds_bytes_per_cu;       /* local data share capacity */
+    int vgprs_per_simd_lane;    /* unified VGPR+AGPR file per lane and SIMD */
+    int max_waves_per_simd;     /* wave slots per SIMD */
+    double clock_ghz;           /* peak engine clock */
+    double mfma_bf16_flops_per_clk_cu; /* dense bf16 MFMA throughput */
+    double valu_lanes_per_clk_simd;    /* fp32 VALU lanes per clock per SIMD */
+    double trans_cycles_per_op;        /* SIMD cycles of one wave-wide v_exp_f32 */
+    double lds_bytes_per_clk_cu;       /* LDS read bandwidth */
+    double l2_bytes_per_clk_xcd;       /* L2 read bandwidth per XCD */
+    double hbm_bytes_per_s;            /* sustained HBM read bandwidth */
+    double hbm_latency_us;             /* loaded HBM latency (for bytes in flight) */
+    double launch_us;                  /* kernel launch + drain overhead */
+} attn_device_desc;
+
+/* Fill *out from the current HIP device (structural properties) and the
+ * built-in gfx950 performance properties.  Without a usable device, fills
+ * the MI355X specification values and returns ATTN_EHIP (out still valid). */
+int attn_query_device(attn_device_desc* out);
+
+/*
+ * Plan query: writes a one-line, human-readable plan -- the named tile
+ * symbols (BLOCK_M, BLOCK_N, WAVES, DBUF for ATTN_KIND_FWD; N_SPLITS, CHUNK,
+ * ... for ATTN_KIND_DECODE), the grid size, the modelled time in us and the
+ * binding resource -- for the given problem into buf (NUL-terminated,
+ * truncated to buflen).  Returns the full length of the line (excluding the
+ * NUL) or a negative ATTN_E* code.  Sq is ignored for decode.  desc may be
+ * NULL (use attn_query_device()).  Host-only; launches nothing.
+ */
+int attn_get_plan(int kind, int B, int H, int Sq, int Skv, int d, int causal, int n_splits,
+                  char* buf, int buflen);
+int attn_get_plan_for(const attn_device_desc* desc, int kind, int B, int H, int Sq, int Skv,
+                      int d, int causal, int n_splits, char* buf, int buflen);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ATTN_H */

@@ -1,0 +1,185 @@
+"""Tiled exact attention on MI355X (gfx950): Python binding of libattn.so.
+
+This module only marshals arguments into the C ABI declared in
+``include/attn.h``; every step of the computation runs in the HIP kernels of
+``libattn.so``.  PyTorch is used for device memory and the current stream.
+There is no fallback: if the library is missing, importing this package
+raises ImportError, and the compute calls raise AttnError without a gfx950
+device.
+
+    o = attn_fwd(q, k, v, scale=None, causal=False)  # q [B,H,Sq,d], k/v [B,H,Skv,d] bf16
+    o = attn_decode(q, k, v, n_splits=0)             # q [B,H,d], k/v [B,H,Skv,d] bf16
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libattn.so")
+
+ATTN_OK = 0
+ATTN_EINVAL = -1
+ATTN_EUNSUPPORTED = -2
+ATTN_EHIP = -3
+ATTN_ENOMEM = -4
+KIND_FWD = 0
+KIND_DECODE = 1
+
+# Entry points declared in include/attn.h.
+EXPORTED = ("attn_fwd", "attn_decode", "attn_set_stream", "attn_get_stream",
+            "attn_last_error", "attn_query_device", "attn_get_plan", "attn_get_plan_for")
+
+
+class AttnError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"attn error {code}: {msg}")
+        self.code = code
+
+
+class DeviceDesc(ctypes.Structure):
+    _fields_ = [
+        ("arch", ctypes.c_char * 32),
+        ("num_cus", ctypes.c_int),
+        ("num_xcds", ctypes.c_int),
+        ("simds_per_cu", ctypes.c_int),
+        ("wave_size", ctypes.c_int),
+        ("lds_bytes_per_cu", ctypes.c_int),
+        ("vgprs_per_simd_lane", ctypes.c_int),
+        ("max_waves_per_simd", ctypes.c_int),
+        ("clock_ghz", ctypes.c_double),
+        ("mfma_bf16_flops_per_clk_cu", ctypes.c_double),
+        ("valu_lanes_per_clk_simd", ctypes.c_double),
+        ("trans_cycles_per_op", ctypes.c_double),
+        ("lds_bytes_per_clk_cu", ctypes.c_double),
+        ("l2_bytes_per_clk_xcd", ctypes.c_double),
+        ("hbm_bytes_per_s", ctypes.c_double),
+        ("hbm_latency_us", ctypes.c_double),
+        ("launch_us", ctypes.c_double),
+    ]
+
+    def as_dict(self) -> dict:
+        d = {name: getattr(self, name) for name, _ in self._fields_}
+        d["arch"] = self.arch.decode()
+        return d
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is not built; run `python paper_2609_29219_amd/build.py` "
+            "(or __graft_entry__.build())")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, ci, cf = ctypes.c_void_p, ctypes.c_int, ctypes.c_float
+    lib.attn_fwd.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, cf, ci]
+    lib.attn_decode.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci]
+    lib.attn_set_stream.argtypes = [vp]
+    lib.attn_get_stream.argtypes = []
+    lib.attn_get_stream.restype = vp
+    lib.attn_last_error.argtypes = []
+    lib.attn_last_error.restype = ctypes.c_char_p
+    lib.attn_query_device.argtypes = [ctypes.POINTER(DeviceDesc)]
+    lib.attn_get_plan.argtypes = [ci, ci, ci, ci, ci, ci, ci, ci, ctypes.c_char_p, ci]
+    lib.attn_get_plan_for.argtypes = [ctypes.POINTER(DeviceDesc), ci, ci, ci, ci, ci, ci, ci,
+                                      ci, ctypes.c_char_p, ci]
+    for fn in (lib.attn_fwd, lib.attn_decode, lib.attn_set_stream, lib.attn_query_device,
+               lib.attn_get_plan, lib.attn_get_plan_for):
+        fn.restype = ci
+    return lib
+
+
+lib = _load()
+
+
+def last_error() -> str:
+    return lib.attn_last_error().decode()
+
+
+def _check(rc: int):
+    if rc != ATTN_OK:
+        raise AttnError(rc, last_error())
+
+
+def _set_stream(t) -> None:
+    import torch
+    lib.attn_set_stream(ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream))
+
+
+def _require(t, dtype, shape, name):
+    import torch
+    if not isinstance(t, torch.Tensor) or t.dtype != dtype or not t.is_cuda:
+        raise TypeError(f"{name} must be a {dtype} tensor on a HIP device")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def attn_fwd(q, k, v, o=None, scale: float | None = None, causal: bool = False):
+    """Prefill attention; returns o fp32 [B,H,Sq,d]."""
+    import torch
+    B, H, Sq, d = q.shape
+    Skv = k.shape[2]
+    _require(q, torch.bfloat16, (B, H, Sq, d), "q")
+    _require(k, torch.bfloat16, (B, H, Skv, d), "k")
+    _require(v, torch.bfloat16, (B, H, Skv, d), "v")
+    if o is None:
+        o = torch.empty((B, H, Sq, d), dtype=torch.float32, device=q.device)
+    _require(o, torch.float32, (B, H, Sq, d), "o")
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    _set_stream(q)
+    _check(lib.attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), B, H, Sq, Skv, d,
+                        float(scale), int(bool(causal))))
+    return o
+
+
+def attn_decode(q, k, v, o=None, n_splits: int = 0):
+    """Split-KV single-query attention; returns o fp32 [B,H,d]."""
+    import torch
+    B, H, d = q.shape
+    Skv = k.shape[2]
+    _require(q, torch.bfloat16, (B, H, d), "q")
+    _require(k, torch.bfloat16, (B, H, Skv, d), "k")
+    _require(v, torch.bfloat16, (B, H, Skv, d), "v")
+    if o is None:
+        o = torch.empty((B, H, d), dtype=torch.float32, device=q.device)
+    _require(o, torch.float32, (B, H, d), "o")
+    _set_stream(q)
+    _check(lib.attn_decode(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), B, H, Skv, d,
+                           int(n_splits)))
+    return o
+
+
+def query_device() -> dict:
+    desc = DeviceDesc()
+    lib.attn_query_device(ctypes.byref(desc))
+    return desc.as_dict()
+
+
+def get_plan(kind: int, B: int, H: int, Sq: int, Skv: int, d: int, causal: bool = False,
+             n_splits: int = 0, desc: DeviceDesc | None = None) -> str:
+    buf = ctypes.create_string_buffer(512)
+    if desc is None:
+        rc = lib.attn_get_plan(kind, B, H, Sq, Skv, d, int(bool(causal)), n_splits, buf, 512)
+    else:
+        rc = lib.attn_get_plan_for(ctypes.byref(desc), kind, B, H, Sq, Skv, d, int(bool(causal)),
+                                   n_splits, buf, 512)
+    if rc < 0:
+        raise AttnError(rc, last_error())
+    return buf.value.decode()
+
+
+def parse_plan(line: str) -> dict:
+    out = {}
+    for tok in line.split():
+        key, _, val = tok.partition("=")
+        try:
+            out[key] = int(val)
+        except ValueError:
+            try:
+                out[key] = float(val)
+            except ValueError:
+                out[key] = val
+    return out

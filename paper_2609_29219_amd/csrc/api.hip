@@ -1,0 +1,282 @@
+// C ABI of libattn.so: argument validation, per-thread stream and error
+// state, plan cache, device description and the decode workspace.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <map>
+#include <mutex>
+#include <string>
+#include <tuple>
+#include <vector>
+
+#include "common.h"
+
+namespace attn {
+hipError_t launch_fwd_d64(const FwdPlan&, const void*, const void*, const void*, float*, int,
+                          int, float, uint32_t, int, hipStream_t);
+hipError_t launch_fwd_d128(const FwdPlan&, const void*, const void*, const void*, float*, int,
+                           int, float, uint32_t, int, hipStream_t);
+
+hipError_t launch_fwd(const FwdPlan& p, const void* q, const void* k, const void* v, float* o,
+                      int B, int H, int Sq, int Skv, float scale, int num_xcds,
+                      hipStream_t stream) {
+    (void)B;
+    (void)H;
+    // softmax in base 2: exp(x) = 2^(x*log2 e); a negative scale is applied
+    // as an exact sign flip of Q so the kernel's scale factor is >= 0
+    const double s = fabs((double)scale) * 1.4426950408889634;
+    const uint32_t q_sign = scale < 0.f ? 0x80008000u : 0u;
+    if (p.d == 64)
+        return launch_fwd_d64(p, q, k, v, o, Sq, Skv, (float)s, q_sign, num_xcds, stream);
+    if (p.d == 128)
+        return launch_fwd_d128(p, q, k, v, o, Sq, Skv, (float)s, q_sign, num_xcds, stream);
+    return hipErrorInvalidValue;
+}
+}  // namespace attn
+
+using namespace attn;
+
+namespace {
+
+thread_local hipStream_t t_stream = nullptr;
+thread_local std::string t_error;
+
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    t_error = buf;
+    return code;
+}
+
+int fail_hip(hipError_t e, const char* what) {
+    return fail(ATTN_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// ---- per-device state --------------------------------------------------
+struct DeviceState {
+    bool ready = false;
+    bool is_gfx950 = false;
+    attn_device_desc desc{};
+    hipMemPool_t pool = nullptr;
+};
+std::mutex g_mu;
+std::map<int, DeviceState> g_devices;
+std::map<std::tuple<int, int, int, int, int, int, int, int>, FwdPlan> g_fwd_cache;
+std::map<std::tuple<int, int, int, int, int, int>, DecodePlan> g_dec_cache;
+
+// Structural properties from the runtime; performance properties from the
+// built-in gfx950 description.
+hipError_t fill_desc(int dev, attn_device_desc* d) {
+    default_desc(d);
+    hipDeviceProp_t prop;
+    hipError_t e = hipGetDeviceProperties(&prop, dev);
+    if (e != hipSuccess) return e;
+    snprintf(d->arch, sizeof d->arch, "%s", prop.gcnArchName);
+    char* colon = strchr(d->arch, ':');
+    if (colon) *colon = 0;
+    d->num_cus = prop.multiProcessorCount;
+    if (prop.maxSharedMemoryPerMultiProcessor > 0)
+        d->lds_bytes_per_cu = (int)prop.maxSharedMemoryPerMultiProcessor;
+    if (prop.clockRate > 0) d->clock_ghz = prop.clockRate / 1e6;
+    return hipSuccess;
+}
+
+int device_state(DeviceState** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail_hip(e, "hipGetDevice");
+    std::lock_guard<std::mutex> lk(g_mu);
+    DeviceState& st = g_devices[dev];
+    if (!st.ready) {
+        e = fill_desc(dev, &st.desc);
+        if (e != hipSuccess) return fail_hip(e, "hipGetDeviceProperties");
+        st.is_gfx950 = strcmp(st.desc.arch, "gfx950") == 0;
+        st.ready = true;
+    }
+    if (!st.is_gfx950)
+        return fail(ATTN_EUNSUPPORTED, "device %d is %s; this library is built for gfx950", dev,
+                    st.desc.arch);
+    *out = &st;
+    return ATTN_OK;
+}
+
+// Optional fixed tile choice for the block-size ablation only:
+// ATTN_FORCE_PLAN="bn=64,waves=4,dbuf=1".  Never used to select tiles.
+bool forced_fwd(int* bn, int* waves, int* dbuf) {
+    const char* s = getenv("ATTN_FORCE_PLAN");
+    if (!s || !*s) return false;
+    return sscanf(s, "bn=%d,waves=%d,dbuf=%d", bn, waves, dbuf) == 3;
+}
+
+int validate_common(const void* q, const void* k, const void* v, const void* o, int B, int H,
+                    int Skv, int d) {
+    if (!q || !k || !v || !o) return fail(ATTN_EINVAL, "null tensor pointer");
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o))
+        return fail(ATTN_EINVAL, "tensor pointers must be 16-byte aligned");
+    if (B <= 0 || H <= 0 || Skv <= 0 || d <= 0)
+        return fail(ATTN_EINVAL, "dimensions must be positive (B=%d H=%d Skv=%d d=%d)", B, H,
+                    Skv, d);
+    if (d != 64 && d != 128) return fail(ATTN_EUNSUPPORTED, "head dim %d not in {64, 128}", d);
+    return ATTN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int attn_set_stream(void* hip_stream) {
+    t_stream = static_cast<hipStream_t>(hip_stream);
+    return ATTN_OK;
+}
+
+void* attn_get_stream(void) { return t_stream; }
+
+const char* attn_last_error(void) { return t_error.c_str(); }
+
+int attn_query_device(attn_device_desc* out) {
+    if (!out) return fail(ATTN_EINVAL, "null descriptor");
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = fill_desc(dev, out);
+    if (e != hipSuccess) {
+        default_desc(out);
+        return fail_hip(e, "no usable HIP device (MI355X specification values returned)");
+    }
+    return ATTN_OK;
+}
+
+int attn_get_plan_for(const attn_device_desc* desc, int kind, int B, int H, int Sq, int Skv,
+                      int d, int causal, int n_splits, char* buf, int buflen) {
+    attn_device_desc local;
+    if (!desc) {
+        attn_query_device(&local);  // falls back to the specification values
+        desc = &local;
+    }
+    if (buflen < 0 || (buflen > 0 && !buf)) return fail(ATTN_EINVAL, "bad output buffer");
+    if (B <= 0 || H <= 0 || Skv <= 0 || d <= 0 || (kind == ATTN_KIND_FWD && Sq <= 0))
+        return fail(ATTN_EINVAL, "dimensions must be positive");
+    if (d != 64 && d != 128) return fail(ATTN_EUNSUPPORTED, "head dim %d not in {64, 128}", d);
+    if (desc->num_cus <= 0 || desc->num_xcds <= 0 || desc->clock_ghz <= 0.0 ||
+        desc->lds_bytes_per_cu <= 0 || desc->hbm_bytes_per_s <= 0.0 ||
+        desc->mfma_bf16_flops_per_clk_cu <= 0.0 || desc->lds_bytes_per_clk_cu <= 0.0 ||
+        desc->l2_bytes_per_clk_xcd <= 0.0 || desc->valu_lanes_per_clk_simd <= 0.0 ||
+        desc->simds_per_cu <= 0 || desc->wave_size <= 0 || desc->vgprs_per_simd_lane <= 0 ||
+        desc->max_waves_per_simd <= 0)
+        return fail(ATTN_EINVAL, "device description has non-positive fields");
+    if (kind == ATTN_KIND_FWD) {
+        if (causal && Sq > Skv) return fail(ATTN_EUNSUPPORTED, "causal needs Sq <= Skv");
+        FwdPlan p;
+        if (!plan_fwd(*desc, B, H, Sq, Skv, d, causal ? 1 : 0, &p))
+            return fail(ATTN_EUNSUPPORTED, "no feasible prefill plan");
+        return format_fwd_plan(p, buf, buflen);
+    }
+    if (kind == ATTN_KIND_DECODE) {
+        DecodePlan p;
+        if (!plan_decode(*desc, B, H, Skv, d, n_splits, &p))
+            return fail(ATTN_EUNSUPPORTED, "no feasible decode plan");
+        return format_decode_plan(p, buf, buflen);
+    }
+    return fail(ATTN_EINVAL, "unknown plan kind %d", kind);
+}
+
+int attn_get_plan(int kind, int B, int H, int Sq, int Skv, int d, int causal, int n_splits,
+                  char* buf, int buflen) {
+    return attn_get_plan_for(nullptr, kind, B, H, Sq, Skv, d, causal, n_splits, buf, buflen);
+}
+
+int attn_fwd(const void* q, const void* k, const void* v, float* o, int B, int H, int Sq,
+             int Skv, int d, float scale, int causal) {
+    int rc = validate_common(q, k, v, o, B, H, Skv, d);
+    if (rc) return rc;
+    if (Sq <= 0) return fail(ATTN_EINVAL, "Sq must be positive (got %d)", Sq);
+    if (!isfinite(scale)) return fail(ATTN_EINVAL, "scale must be finite");
+    if (causal && Sq > Skv)
+        return fail(ATTN_EUNSUPPORTED, "causal attention needs Sq <= Skv (Sq=%d Skv=%d)", Sq, Skv);
+    DeviceState* st = nullptr;
+    rc = device_state(&st);
+    if (rc) return rc;
+
+    const int c = causal ? 1 : 0;
+    FwdPlan plan;
+    int fbn, fw, fdb;
+    if (forced_fwd(&fbn, &fw, &fdb)) {
+        if (!plan_fwd_fixed(st->desc, B, H, Sq, Skv, d, c, fbn, fw, fdb, &plan))
+            return fail(ATTN_EINVAL, "ATTN_FORCE_PLAN names an infeasible or unknown tile");
+    } else {
+        std::lock_guard<std::mutex> lk(g_mu);
+        auto key = std::make_tuple(B, H, Sq, Skv, d, c, st->desc.num_cus, 0);
+        auto it = g_fwd_cache.find(key);
+        if (it != g_fwd_cache.end()) {
+            plan = it->second;
+        } else {
+            if (!plan_fwd(st->desc, B, H, Sq, Skv, d, c, &plan))
+                return fail(ATTN_EUNSUPPORTED, "no feasible prefill plan for this shape");
+            g_fwd_cache[key] = plan;
+        }
+    }
+    hipError_t e = launch_fwd(plan, q, k, v, o, B, H, Sq, Skv, scale, st->desc.num_xcds, t_stream);
+    if (e != hipSuccess) return fail_hip(e, "prefill launch");
+    return ATTN_OK;
+}
+
+int attn_decode(const void* q, const void* k, const void* v, float* o, int B, int H, int Skv,
+                int d, int n_splits) {
+    int rc = validate_common(q, k, v, o, B, H, Skv, d);
+    if (rc) return rc;
+    DeviceState* st = nullptr;
+    rc = device_state(&st);
+    if (rc) return rc;
+    DecodePlan plan;
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        auto key = std::make_tuple(B, H, Skv, d, n_splits, st->desc.num_cus);
+        auto it = g_dec_cache.find(key);
+        if (it != g_dec_cache.end()) {
+            plan = it->second;
+        } else {
+            if (!plan_decode(st->desc, B, H, Skv, d, n_splits, &plan))
+                return fail(ATTN_EUNSUPPORTED, "no feasible decode plan for this shape");
+            g_dec_cache[key] = plan;
+        }
+        if (!st->pool) {
+            int dev = 0;
+            hipGetDevice(&dev);
+            hipMemPoolProps props;
+            memset(&props, 0, sizeof props);
+            props.allocType = hipMemAllocationTypePinned;
+            props.location.type = hipMemLocationTypeDevice;
+            props.location.id = dev;
+            hipError_t e = hipMemPoolCreate(&st->pool, &props);
+            if (e != hipSuccess) {
+                st->pool = nullptr;
+                return fail_hip(e, "hipMemPoolCreate");
+            }
+            uint64_t keep = UINT64_MAX;  // keep freed blocks for reuse
+            hipMemPoolSetAttribute(st->pool, hipMemPoolAttrReleaseThreshold, &keep);
+        }
+    }
+    const size_t ws_bytes = (size_t)B * H * plan.n_splits * (d + 2) * sizeof(float);
+    void* ws = nullptr;
+    hipError_t e = hipMallocFromPoolAsync(&ws, ws_bytes, st->pool, t_stream);
+    if (e != hipSuccess || !ws) {
+        (void)hipGetLastError();
+        return fail(ATTN_ENOMEM, "decode workspace of %zu bytes: %s", ws_bytes,
+                    hipGetErrorString(e));
+    }
+    const float scale = (float)(1.0 / sqrt((double)d));
+    e = launch_decode(plan, q, k, v, o, static_cast<float*>(ws), B, H, Skv, scale, t_stream);
+    hipError_t e2 = hipFreeAsync(ws, t_stream);
+    if (e != hipSuccess) return fail_hip(e, "decode launch");
+    if (e2 != hipSuccess) return fail_hip(e2, "decode workspace free");
+    return ATTN_OK;
+}
+
+}  // extern "C"

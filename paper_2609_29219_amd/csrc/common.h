@@ -1,0 +1,74 @@
+// Internal declarations shared by the translation units of libattn.so.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "attn.h"
+
+namespace attn {
+
+// ---------------------------------------------------------------- plans --
+// Tile symbols of the prefill kernel, named as the planner reports them.
+struct FwdPlan {
+    int d = 0;
+    int block_m = 0;    // queries per workgroup (32 per wave)
+    int block_n = 0;    // keys per K/V tile staged in LDS
+    int waves = 0;      // waves per workgroup
+    int dbuf = 0;       // 1: two LDS slots, next tile prefetched during compute
+    int causal = 0;
+    int lds_bytes = 0;  // per workgroup
+    int vgprs = 0;      // modelled VGPRs per lane
+    int wg_per_cu = 0;  // modelled occupancy
+    long long grid = 0;
+    int n_qtiles = 0;
+    double modeled_us = 0.0;
+    const char* bound = "";  // resource that binds the modelled time
+};
+
+// Symbols of the decode pair (partial + combine).
+struct DecodePlan {
+    int d = 0;
+    int n_splits = 0;  // effective split count (every split non-empty)
+    int chunk = 0;     // keys per split
+    int threads = 0;   // threads per partial workgroup
+    int unroll = 0;    // keys per lane group per loop step
+    int wg_per_cu = 0;
+    long long grid = 0;
+    double modeled_us = 0.0;
+    const char* bound = "";
+};
+
+// Candidate domains: every point is an instantiated kernel.
+constexpr int kFwdBlockN[] = {32, 64, 128};
+constexpr int kFwdWaves[] = {4, 8};
+constexpr int kFwdDbuf[] = {0, 1};
+constexpr int kDecodeThreads = 256;
+constexpr int kDecodeUnroll = 8;
+
+// LDS footprint of a prefill workgroup: K tile [BN][D+8] and V^T tile
+// [D][BN+8] in bf16, times two slots when double buffered.
+constexpr int fwd_lds_bytes(int d, int bn, int dbuf) {
+    return (dbuf ? 2 : 1) * (bn * (d + 8) + d * (bn + 8)) * 2;
+}
+
+// Planner (host only, pure arithmetic on the device description).
+void default_desc(attn_device_desc* out);
+bool plan_fwd(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d, int causal,
+              FwdPlan* out);
+bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d,
+                    int causal, int bn, int waves, int dbuf, FwdPlan* out);
+bool plan_decode(const attn_device_desc& desc, int B, int H, int Skv, int d, int n_splits,
+                 DecodePlan* out);
+int format_fwd_plan(const FwdPlan& p, char* buf, int buflen);
+int format_decode_plan(const DecodePlan& p, char* buf, int buflen);
+
+// Launchers (defined next to the kernels).
+hipError_t launch_fwd(const FwdPlan& p, const void* q, const void* k, const void* v, float* o,
+                      int B, int H, int Sq, int Skv, float scale, int num_xcds,
+                      hipStream_t stream);
+hipError_t launch_decode(const DecodePlan& p, const void* q, const void* k, const void* v,
+                         float* o, float* workspace, int B, int H, int Skv, float scale,
+                         hipStream_t stream);
+
+}  // namespace attn

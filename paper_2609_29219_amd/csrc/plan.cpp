@@ -1,0 +1,280 @@
+// Analytic tile/split planner: no autotuning, no measurement in the loop.
+//
+// The paper keeps block sizes and pipeline knobs symbolic and picks them by
+// minimising a latency expression assembled over a Hierarchical Execution
+// Graph (HEG) under resource constraints (latency-modelling section:
+// sequential composition adds, Eq. heg-seq; a for node multiplies by its
+// trip count, Eq. heg-for; a pipe node with load/body/store stages takes a
+// sum or a max depending on a two-bit knob, Eq. heg-pipe; the candidate is
+// the constrained argmin, Eq. heg-optimization, and the best feasible
+// candidate wins, Eq. global-candidate-selection).  The architecture
+// description supplies primitive costs and capacities (architecture
+// description section).
+//
+// Here the domain is tiny (3 tile widths x 2 wave counts x 2 pipeline knobs
+// for prefill; a few dozen split counts for decode), so exhaustive
+// enumeration returns the exact argmin a solver would.  The prefill HEG is
+//     seq( load Q ; for(n_tiles, pipe(load K/V tile, body, -)) ; store O )
+// with body = S = K Q^T, softmax update, O += V^T P^T, and the decode HEG is
+//     seq( for(steps, pipe(load K/V keys, local softmax, -)) ; merge ;
+//          combine (gather partials, global softmax, final output) ).
+// The grid is regular except for causal prefill, whose triangular work is
+// regularised by summing per-tile work over the grid plus a tail term (the
+// paper's scope paragraph asks for exactly this kind of regularisation).
+#include <math.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+
+#include "common.h"
+
+namespace attn {
+
+void default_desc(attn_device_desc* d) {
+    memset(d, 0, sizeof *d);
+    snprintf(d->arch, sizeof d->arch, "gfx950");
+    // structural properties (MI355X specification)
+    d->num_cus = 256;
+    d->num_xcds = 8;
+    d->simds_per_cu = 4;
+    d->wave_size = 64;
+    d->lds_bytes_per_cu = 160 * 1024;
+    d->vgprs_per_simd_lane = 512;
+    d->max_waves_per_simd = 8;
+    d->clock_ghz = 2.4;
+    // performance properties (per-CU primitive rates)
+    d->mfma_bf16_flops_per_clk_cu = 4096.0;  // 32x32x16 bf16 MFMA: 32 cycles per SIMD
+    d->valu_lanes_per_clk_simd = 16.0;       // a wave64 fp32 op occupies 4 cycles
+    d->trans_cycles_per_op = 16.0;           // a wave64 v_exp_f32 occupies 16 cycles
+    d->lds_bytes_per_clk_cu = 128.0;
+    d->l2_bytes_per_clk_xcd = 2048.0;
+    d->hbm_bytes_per_s = 6.0e12;             // sustained stream read
+    d->hbm_latency_us = 2.0;
+    d->launch_us = 4.0;
+}
+
+namespace {
+
+// HEG composition rules.
+double heg_pipe(double load, double body, double store, int b_lm, int b_ms) {
+    if (!b_lm && !b_ms) return load + body + store;
+    if (!b_lm && b_ms) return std::max(load + body, store);
+    if (b_lm && !b_ms) return std::max(load, body + store);
+    return std::max(load, std::max(body, store));
+}
+double heg_for(double trips, double body) { return trips * body; }
+
+int round_up(int x, int a) { return (x + a - 1) / a * a; }
+
+struct FwdCost {
+    double total_cycles;
+    const char* bound;
+};
+
+// VGPRs per lane of one prefill wave (Q operand, score and output
+// accumulators, bf16 probabilities, prefetch registers, scalars/addresses).
+int fwd_vgprs(int d, int bn, int waves, int dbuf) {
+    const int nt = waves * 64;
+    const int kch = (bn * d / 8 + nt - 1) / nt;
+    const int vch = ((bn / 4) * (d / 8) + nt - 1) / nt;
+    const int prefetch = kch * 4 + vch * 16;
+    int v = d / 4 + bn / 2 + d / 2 + bn / 4 + (dbuf ? prefetch : prefetch / 2) + 24;
+    return round_up(v, 8);
+}
+
+}  // namespace
+
+bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d,
+                    int causal, int bn, int waves, int dbuf, FwdPlan* out) {
+    FwdPlan p;
+    p.d = d;
+    p.block_n = bn;
+    p.waves = waves;
+    p.dbuf = dbuf;
+    p.causal = causal;
+    p.block_m = 32 * waves;
+    p.lds_bytes = fwd_lds_bytes(d, bn, dbuf);
+    p.vgprs = fwd_vgprs(d, bn, waves, dbuf);
+    // legality: capacities and primitive validity
+    if (bn % 32 != 0 || d % 32 != 0) return false;
+    if (p.lds_bytes > desc.lds_bytes_per_cu) return false;
+    if (p.vgprs > desc.vgprs_per_simd_lane) return false;
+    const int simds = desc.simds_per_cu;
+    const int waves_per_simd_wg = std::max(1, waves / simds);
+    const int wpe_regs = desc.vgprs_per_simd_lane / p.vgprs;  // waves per SIMD by registers
+    int wg = desc.lds_bytes_per_cu / p.lds_bytes;
+    wg = std::min(wg, (wpe_regs * simds) / waves);
+    wg = std::min(wg, (desc.max_waves_per_simd * simds) / waves);
+    if (wg < 1) return false;
+    p.wg_per_cu = wg;
+    p.n_qtiles = (Sq + p.block_m - 1) / p.block_m;
+    p.grid = (long long)B * H * p.n_qtiles;
+    if (p.grid > 0x7fffffffLL) return false;
+
+    const double bm = p.block_m;
+    const int cus_per_xcd = std::max(1, desc.num_cus / std::max(1, desc.num_xcds));
+    const double l2_share = desc.l2_bytes_per_clk_xcd / cus_per_xcd;  // bytes/clk per CU
+    // ---- primitive costs of one K/V tile for the wg workgroups of a CU -----
+    const double mfma = wg * 4.0 * bm * bn * d / desc.mfma_bf16_flops_per_clk_cu;
+    const double valu_op = desc.wave_size / desc.valu_lanes_per_clk_simd;  // cycles per op
+    const double scores_per_lane = 32.0 * bn / desc.wave_size;
+    const double wave_valu = scores_per_lane * (4.5 * valu_op + desc.trans_cycles_per_op) +
+                             (24.0 + 0.1 * d / 2.0) * valu_op;
+    const double valu = wg * waves_per_simd_wg * wave_valu;  // per SIMD
+    const double lds_rd = wg * waves * 4.0 * bn * d / desc.lds_bytes_per_clk_cu;
+    const double lds_wr = wg * 4.0 * bn * d / desc.lds_bytes_per_clk_cu;
+    const double glob = wg * 4.0 * bn * d / l2_share;
+    const int wps = wg * waves_per_simd_wg;  // waves sharing a SIMD
+    double body = std::max(std::max(mfma, valu), lds_rd + lds_wr);
+    if (wps < 2) body = mfma + valu;  // one wave: the S->softmax->PV chain serialises
+    else body += 0.2 * std::min(mfma, valu);
+    const double tile = heg_pipe(glob, body, 0.0, dbuf, 0);
+    const double load_q = wg * bm * d * 2.0 / l2_share + glob;
+    const double store_o = wg * bm * d * 4.0 / l2_share;
+
+    // ---- grid: regular (non-causal) or regularised (causal) --------------
+    const double slots = (double)desc.num_cus * wg;
+    const int full_tiles = (Skv + bn - 1) / bn;
+    double cycles;
+    if (!causal) {
+        const double rounds = ceil((double)p.grid / slots);
+        cycles = rounds * (load_q + heg_for(full_tiles, tile) + store_o);
+    } else {
+        // sum of per-q-tile work over one head, times B*H, spread over the slots
+        double sum_tiles = 0.0;
+        int max_tiles = 0;
+        for (int qt = 0; qt < p.n_qtiles; ++qt) {
+            const int last_q = std::min(qt * p.block_m + p.block_m - 1, Sq - 1);
+            const int kv_end = std::min(Skv, last_q + (Skv - Sq) + 1);
+            const int nt = (kv_end + bn - 1) / bn;
+            sum_tiles += nt;
+            max_tiles = std::max(max_tiles, nt);
+        }
+        const double per_wg_fixed = load_q + store_o;
+        const double work = (double)B * H * (sum_tiles * tile + p.n_qtiles * per_wg_fixed);
+        const double longest = per_wg_fixed + heg_for(max_tiles, tile);
+        cycles = (p.grid > slots) ? work / slots + 0.5 * longest : longest;
+    }
+    double us = cycles / (desc.clock_ghz * 1e3);
+    const double bytes = (double)B * H * ((double)Sq * d * 6.0 + (double)Skv * d * 4.0);
+    const double hbm_us = bytes / desc.hbm_bytes_per_s * 1e6;
+    const char* bound;
+    if (hbm_us > us) {
+        us = hbm_us;
+        bound = "hbm";
+    } else if (dbuf && glob > body) {
+        bound = "l2";
+    } else if (wps < 2) {
+        bound = "mfma+valu";
+    } else if (mfma >= valu && mfma >= lds_rd + lds_wr) {
+        bound = "mfma";
+    } else if (valu >= lds_rd + lds_wr) {
+        bound = "valu";
+    } else {
+        bound = "lds";
+    }
+    p.modeled_us = us + desc.launch_us;
+    p.bound = bound;
+    *out = p;
+    return true;
+}
+
+bool plan_fwd(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d, int causal,
+              FwdPlan* out) {
+    bool found = false;
+    FwdPlan best;
+    for (int bn : kFwdBlockN)
+        for (int waves : kFwdWaves)
+            for (int dbuf : kFwdDbuf) {
+                FwdPlan p;
+                if (!plan_fwd_fixed(desc, B, H, Sq, Skv, d, causal, bn, waves, dbuf, &p)) continue;
+                // strict improvement keeps the first (smallest) candidate on ties
+                if (!found || p.modeled_us < best.modeled_us * (1.0 - 1e-9)) {
+                    best = p;
+                    found = true;
+                }
+            }
+    if (found) *out = best;
+    return found;
+}
+
+bool plan_decode(const attn_device_desc& desc, int B, int H, int Skv, int d, int n_req,
+                 DecodePlan* out) {
+    const int nt = kDecodeThreads, unroll = kDecodeUnroll;
+    const int groups = nt / (d / 8);       // keys per workgroup step
+    const int step_keys = groups * unroll;  // keys per loop iteration
+    const long long BH = (long long)B * H;
+    const double cu_share = desc.hbm_bytes_per_s / desc.num_cus;  // bytes/s per CU
+    const int max_wg_cu = std::max(1, desc.max_waves_per_simd * desc.simds_per_cu / (nt / 64));
+
+    auto model = [&](int n, DecodePlan* p) -> bool {
+        const int chunk = (Skv + n - 1) / n;
+        const int n_eff = (Skv + chunk - 1) / chunk;
+        const long long grid = BH * n_eff;
+        if (grid > 0x7fffffffLL) return false;
+        const double wg_bytes = (double)chunk * d * 4.0;
+        const double per_cu = ceil((double)grid / desc.num_cus);  // workgroups per CU
+        const double resident = std::min<double>(per_cu, max_wg_cu);
+        // bytes in flight per CU: every lane keeps 2*unroll 16-byte loads open
+        const double inflight = resident * nt * 2.0 * unroll * 16.0;
+        const double cu_bw = std::min(cu_share, inflight / (desc.hbm_latency_us * 1e-6));
+        // for(steps, pipe(load, local softmax)): load-bound, loads overlap compute
+        const double steps = ceil((double)chunk / step_keys);
+        const double stream_us = per_cu * wg_bytes / cu_bw * 1e6;
+        const double merge_us = ceil(per_cu / resident) * 1.0;  // LDS merge + write, ~1 us
+        const double combine_bytes = (double)BH * n_eff * (d + 2) * 4.0 + BH * d * 4.0;
+        const double combine_us = desc.launch_us + combine_bytes / desc.hbm_bytes_per_s * 1e6 +
+                                  n_eff * 0.01;
+        p->d = d;
+        p->n_splits = n_eff;
+        p->chunk = chunk;
+        p->threads = nt;
+        p->unroll = unroll;
+        p->wg_per_cu = (int)resident;
+        p->grid = grid;
+        p->modeled_us = desc.launch_us + stream_us + merge_us + combine_us;
+        p->bound = (cu_bw < cu_share) ? "hbm-latency" : "hbm";
+        (void)steps;
+        return true;
+    };
+
+    if (n_req > 0) {
+        DecodePlan p;
+        if (!model(std::min(n_req, Skv), &p)) return false;
+        *out = p;
+        return true;
+    }
+    static const int cand[] = {1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48, 64, 96, 128, 192, 256, 384, 512};
+    bool found = false;
+    DecodePlan best;
+    for (int n : cand) {
+        if (n > 1 && (Skv + n - 1) / n < step_keys) break;  // at least one full step per split
+        DecodePlan p;
+        if (!model(n, &p)) continue;
+        if (!found || p.modeled_us < best.modeled_us * (1.0 - 1e-9)) {
+            best = p;
+            found = true;
+        }
+    }
+    if (found) *out = best;
+    return found;
+}
+
+int format_fwd_plan(const FwdPlan& p, char* buf, int buflen) {
+    return snprintf(buf, buf ? (size_t)buflen : 0,
+                    "kind=fwd d=%d BLOCK_M=%d BLOCK_N=%d WAVES=%d DBUF=%d causal=%d grid=%lld "
+                    "n_qtiles=%d lds_bytes=%d vgprs=%d wg_per_cu=%d modeled_us=%.3f bound=%s",
+                    p.d, p.block_m, p.block_n, p.waves, p.dbuf, p.causal, p.grid, p.n_qtiles,
+                    p.lds_bytes, p.vgprs, p.wg_per_cu, p.modeled_us, p.bound);
+}
+
+int format_decode_plan(const DecodePlan& p, char* buf, int buflen) {
+    return snprintf(buf, buf ? (size_t)buflen : 0,
+                    "kind=decode d=%d N_SPLITS=%d CHUNK=%d THREADS=%d UNROLL=%d grid=%lld "
+                    "wg_per_cu=%d modeled_us=%.3f bound=%s",
+                    p.d, p.n_splits, p.chunk, p.threads, p.unroll, p.grid, p.wg_per_cu,
+                    p.modeled_us, p.bound);
+}
+
+}  // namespace attn
