@@ -120,6 +120,14 @@ typedef struct attn_device_desc {
  * the MI355X specification values and returns ATTN_EHIP (out still valid). */
 int attn_query_device(attn_device_desc* out);
 
+/* Characterise the current device: fills the structural fields as
+ * attn_query_device() does, then runs isolated microbenchmarks (MFMA, fp32
+ * VALU, v_exp_f32, LDS read and HBM stream rates; about a second, allocates
+ * and frees 2 GiB of device memory, synchronises the device) and stores the
+ * measured performance properties in *out.  The planner's built-in gfx950
+ * values were collected this way once; this call re-measures them. */
+int attn_measure_device(attn_device_desc* out);
+
 /*
  * Plan query: writes a one-line, human-readable plan -- the named tile
  * symbols (BLOCK_M, BLOCK_N, WAVES, DBUF for ATTN_KIND_FWD; N_SPLITS, CHUNK,

@@ -29,7 +29,8 @@ KIND_DECODE = 1
 
 # Entry points declared in include/attn.h.
 EXPORTED = ("attn_fwd", "attn_decode", "attn_set_stream", "attn_get_stream",
-            "attn_last_error", "attn_query_device", "attn_get_plan", "attn_get_plan_for")
+            "attn_last_error", "attn_query_device", "attn_measure_device", "attn_get_plan",
+            "attn_get_plan_for")
 
 
 class AttnError(RuntimeError):
@@ -80,11 +81,12 @@ def _load() -> ctypes.CDLL:
     lib.attn_last_error.argtypes = []
     lib.attn_last_error.restype = ctypes.c_char_p
     lib.attn_query_device.argtypes = [ctypes.POINTER(DeviceDesc)]
+    lib.attn_measure_device.argtypes = [ctypes.POINTER(DeviceDesc)]
     lib.attn_get_plan.argtypes = [ci, ci, ci, ci, ci, ci, ci, ci, ctypes.c_char_p, ci]
     lib.attn_get_plan_for.argtypes = [ctypes.POINTER(DeviceDesc), ci, ci, ci, ci, ci, ci, ci,
                                       ci, ctypes.c_char_p, ci]
     for fn in (lib.attn_fwd, lib.attn_decode, lib.attn_set_stream, lib.attn_query_device,
-               lib.attn_get_plan, lib.attn_get_plan_for):
+               lib.attn_measure_device, lib.attn_get_plan, lib.attn_get_plan_for):
         fn.restype = ci
     return lib
 
@@ -155,6 +157,13 @@ def attn_decode(q, k, v, o=None, n_splits: int = 0):
 def query_device() -> dict:
     desc = DeviceDesc()
     lib.attn_query_device(ctypes.byref(desc))
+    return desc.as_dict()
+
+
+def measure_device() -> dict:
+    """Run the device microbenchmarks (needs a gfx950 device)."""
+    desc = DeviceDesc()
+    _check(lib.attn_measure_device(ctypes.byref(desc)))
     return desc.as_dict()
 
 

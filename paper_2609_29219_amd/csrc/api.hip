@@ -1,5 +1,6 @@
 // C ABI of libattn.so: argument validation, per-thread stream and error
 // state, plan cache, device description and the decode workspace.
+#include <float.h>
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
@@ -20,14 +21,33 @@ hipError_t launch_fwd_d64(const FwdPlan&, const void*, const void*, const void*,
 hipError_t launch_fwd_d128(const FwdPlan&, const void*, const void*, const void*, float*, int,
                            int, float, uint32_t, int, hipStream_t);
 
+bool fwd_resources_d64(int bn, int waves, int dbuf, int causal, KernelRes* r);
+bool fwd_resources_d128(int bn, int waves, int dbuf, int causal, KernelRes* r);
+
+bool fwd_resources(int d, int bn, int waves, int dbuf, int causal, KernelRes* r) {
+    if (d == 64) return fwd_resources_d64(bn, waves, dbuf, causal, r);
+    if (d == 128) return fwd_resources_d128(bn, waves, dbuf, causal, r);
+    return false;
+}
+
+// Forced tiles (ablation only) may run a variant that spills: slow, not wrong.
+bool fwd_resources_forced(int d, int bn, int waves, int dbuf, int causal, KernelRes* r) {
+    if (!fwd_resources(d, bn, waves, dbuf, causal, r)) return false;
+    r->scratch_bytes = 0;
+    return true;
+}
+
 hipError_t launch_fwd(const FwdPlan& p, const void* q, const void* k, const void* v, float* o,
                       int B, int H, int Sq, int Skv, float scale, int num_xcds,
                       hipStream_t stream) {
     (void)B;
     (void)H;
     // softmax in base 2: exp(x) = 2^(x*log2 e); a negative scale is applied
-    // as an exact sign flip of Q so the kernel's scale factor is >= 0
-    const double s = fabs((double)scale) * 1.4426950408889634;
+    // as an exact sign flip of Q.  The kernel needs a factor > 0 (masked
+    // scores are -inf); a zero scale becomes the smallest normal float, with
+    // which every exponent rounds to 0 and the weights are exactly equal.
+    double s = fabs((double)scale) * 1.4426950408889634;
+    if (s < (double)FLT_MIN) s = (double)FLT_MIN;
     const uint32_t q_sign = scale < 0.f ? 0x80008000u : 0u;
     if (p.d == 64)
         return launch_fwd_d64(p, q, k, v, o, Sq, Skv, (float)s, q_sign, num_xcds, stream);
@@ -153,11 +173,26 @@ int attn_query_device(attn_device_desc* out) {
     return ATTN_OK;
 }
 
+int attn_measure_device(attn_device_desc* out) {
+    if (!out) return fail(ATTN_EINVAL, "null descriptor");
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = fill_desc(dev, out);
+    if (e != hipSuccess) return fail_hip(e, "no usable HIP device");
+    e = measure_device(out);
+    if (e != hipSuccess) return fail_hip(e, "device microbenchmarks");
+    return ATTN_OK;
+}
+
 int attn_get_plan_for(const attn_device_desc* desc, int kind, int B, int H, int Sq, int Skv,
                       int d, int causal, int n_splits, char* buf, int buflen) {
     attn_device_desc local;
+    FwdResFn res = nullptr;
     if (!desc) {
-        attn_query_device(&local);  // falls back to the specification values
+        // the current device (compiled kernels' real footprint), else the
+        // specification values
+        if (attn_query_device(&local) == ATTN_OK && strcmp(local.arch, "gfx950") == 0)
+            res = fwd_resources;
         desc = &local;
     }
     if (buflen < 0 || (buflen > 0 && !buf)) return fail(ATTN_EINVAL, "bad output buffer");
@@ -174,7 +209,7 @@ int attn_get_plan_for(const attn_device_desc* desc, int kind, int B, int H, int 
     if (kind == ATTN_KIND_FWD) {
         if (causal && Sq > Skv) return fail(ATTN_EUNSUPPORTED, "causal needs Sq <= Skv");
         FwdPlan p;
-        if (!plan_fwd(*desc, B, H, Sq, Skv, d, causal ? 1 : 0, &p))
+        if (!plan_fwd(*desc, B, H, Sq, Skv, d, causal ? 1 : 0, &p, res))
             return fail(ATTN_EUNSUPPORTED, "no feasible prefill plan");
         return format_fwd_plan(p, buf, buflen);
     }
@@ -208,7 +243,8 @@ int attn_fwd(const void* q, const void* k, const void* v, float* o, int B, int H
     FwdPlan plan;
     int fbn, fw, fdb;
     if (forced_fwd(&fbn, &fw, &fdb)) {
-        if (!plan_fwd_fixed(st->desc, B, H, Sq, Skv, d, c, fbn, fw, fdb, &plan))
+        if (!plan_fwd_fixed(st->desc, B, H, Sq, Skv, d, c, fbn, fw, fdb, &plan,
+                            fwd_resources_forced))
             return fail(ATTN_EINVAL, "ATTN_FORCE_PLAN names an infeasible or unknown tile");
     } else {
         std::lock_guard<std::mutex> lk(g_mu);
@@ -217,7 +253,7 @@ int attn_fwd(const void* q, const void* k, const void* v, float* o, int B, int H
         if (it != g_fwd_cache.end()) {
             plan = it->second;
         } else {
-            if (!plan_fwd(st->desc, B, H, Sq, Skv, d, c, &plan))
+            if (!plan_fwd(st->desc, B, H, Sq, Skv, d, c, &plan, fwd_resources))
                 return fail(ATTN_EUNSUPPORTED, "no feasible prefill plan for this shape");
             g_fwd_cache[key] = plan;
         }

@@ -46,22 +46,37 @@ constexpr int kFwdDbuf[] = {0, 1};
 constexpr int kDecodeThreads = 256;
 constexpr int kDecodeUnroll = 8;
 
-// LDS footprint of a prefill workgroup: K tile [BN][D+8] and V^T tile
-// [D][BN+8] in bf16, times two slots when double buffered.
+// LDS footprint of a prefill workgroup: K tile [BN][D+8] and V tile
+// [BN][D+16] in bf16, times two slots when double buffered.
 constexpr int fwd_lds_bytes(int d, int bn, int dbuf) {
-    return (dbuf ? 2 : 1) * (bn * (d + 8) + d * (bn + 8)) * 2;
+    return (dbuf ? 2 : 1) * (bn * (d + 8) + bn * (d + 32)) * 2;
 }
 
-// Planner (host only, pure arithmetic on the device description).
+// Resource usage of one compiled prefill variant, as the runtime reports it:
+// resident workgroups per CU (registers and LDS together) and private
+// (scratch) bytes per lane.  A variant that spills is not a valid primitive.
+struct KernelRes {
+    int wg_per_cu = 0;
+    int scratch_bytes = 0;
+    int vgprs = 0;
+};
+typedef bool (*FwdResFn)(int d, int bn, int waves, int dbuf, int causal, KernelRes* out);
+
+// Planner (host only, pure arithmetic on the device description).  With
+// res == nullptr (no device) the register footprint is estimated.
 void default_desc(attn_device_desc* out);
 bool plan_fwd(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d, int causal,
-              FwdPlan* out);
+              FwdPlan* out, FwdResFn res = nullptr);
 bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d,
-                    int causal, int bn, int waves, int dbuf, FwdPlan* out);
+                    int causal, int bn, int waves, int dbuf, FwdPlan* out,
+                    FwdResFn res = nullptr);
+bool fwd_resources(int d, int bn, int waves, int dbuf, int causal, KernelRes* out);
 bool plan_decode(const attn_device_desc& desc, int B, int H, int Skv, int d, int n_splits,
                  DecodePlan* out);
 int format_fwd_plan(const FwdPlan& p, char* buf, int buflen);
 int format_decode_plan(const DecodePlan& p, char* buf, int buflen);
+
+hipError_t measure_device(attn_device_desc* d);
 
 // Launchers (defined next to the kernels).
 hipError_t launch_fwd(const FwdPlan& p, const void* q, const void* k, const void* v, float* o,

@@ -43,4 +43,36 @@ hipError_t launch_fwd_d128(const FwdPlan& p, const void* q, const void* k, const
     return hipErrorInvalidValue;
 }
 
+template <int BN, int NW, bool DBUF, bool CAUSAL>
+static bool resources_one(KernelRes* r) {
+    const void* fn = reinterpret_cast<const void*>(&fwd_kernel<128, BN, NW, DBUF, CAUSAL>);
+    hipFuncAttributes a;
+    if (hipFuncGetAttributes(&a, fn) != hipSuccess) return false;
+    int blocks = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, fn, NW * 64, 0) != hipSuccess)
+        return false;
+    r->wg_per_cu = blocks;
+    r->scratch_bytes = (int)a.localSizeBytes;
+    r->vgprs = a.numRegs;
+    return true;
+}
+
+bool fwd_resources_d128(int bn, int waves, int dbuf, int causal, KernelRes* r) {
+#define ATTN_RES(BN, NW)                                                                     \
+    if (bn == BN && waves == NW) {                                                           \
+        if (dbuf) return causal ? resources_one<BN, NW, true, true>(r)                      \
+                                : resources_one<BN, NW, true, false>(r);                    \
+        return causal ? resources_one<BN, NW, false, true>(r)                               \
+                      : resources_one<BN, NW, false, false>(r);                             \
+    }
+    ATTN_RES(32, 4)
+    ATTN_RES(32, 8)
+    ATTN_RES(64, 4)
+    ATTN_RES(64, 8)
+    ATTN_RES(128, 4)
+    ATTN_RES(128, 8)
+#undef ATTN_RES
+    return false;
+}
+
 }  // namespace attn

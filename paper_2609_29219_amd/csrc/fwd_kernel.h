@@ -6,45 +6,71 @@
 //
 // Operand orientation.  Each wave owns 32 query rows and computes the
 // transposed score block S^T = K Q^T with v_mfma_f32_32x32x16_bf16
-// (A = 32 keys x 16 dims from LDS, B = 16 dims x 32 queries held in VGPRs).
-// The 32x32 accumulator puts one query column in each lane (lane & 31) and
-// 16 keys of it in that lane's 16 registers (the other 16 keys sit in lane
-// ^ 32).  The row max and row sum are therefore in-lane reductions plus one
-// exchange between the two wave halves.
+// (A = 32 keys x 16 dims read from LDS, B = 16 dims x 32 queries held in
+// VGPRs).  The 32x32 accumulator puts one query column in each lane
+// (lane & 31) and 16 keys of it in that lane's 16 registers (the other 16
+// keys sit in lane ^ 32).  Row max and row sum are in-lane reductions plus
+// one exchange between the wave halves (v_permlane32_swap).
 //
 // Key permutation.  Accumulator register r of lane half h holds MFMA row
 // 8*(r/4) + 4*h + r%4.  K rows are written to LDS permuted inside each
 // 32-key block (LDS row p holds key 16*((p%8)/4) + 4*(p/8) + p%4), so
 // register r of half h is key 16*h + r: a lane's 16 probabilities are 16
-// consecutive keys, which is exactly the k-operand layout the PV MFMA needs.
+// consecutive keys, which is the k-operand layout the PV MFMA needs.
 //
-// PV.  O^T += V^T P^T with A = V^T (32 dims x 16 keys) read from a
-// transposed V tile in LDS and B = the bf16 probabilities straight from
-// registers.  The output accumulator again has one query per lane, so the
-// online-softmax rescale is one per-lane scalar.
+// PV.  O^T += V^T P^T with B = the bf16 probabilities straight from
+// registers and A = V^T (32 dims x 16 keys).  V stays row-major in LDS and
+// the A operand is fetched with ds_read_b64_tr_b16: inside each 16-lane
+// group, lane i addresses 4 consecutive values E[i][0..3] and lane 4a+b
+// receives E[a][b], E[a+4][b], E[a+8][b], E[a+12][b].  Lane i points at
+// row k0 + i/4, column base + 4*(i%4), so lane j receives the 4 keys
+// k0..k0+3 of column base + j; two such reads give the 8 keys of one MFMA.
+// The output accumulator holds one query per lane, so the online-softmax
+// rescale is one per-lane scalar.
 //
-// Pipelining (the HEG pipe knob on the load/body boundary): DBUF = 1 keeps
-// two LDS slots and issues the global loads of tile t+1 before computing
-// tile t; DBUF = 0 loads, waits and computes in sequence.
+// LDS layout (64 banks of 4 bytes).  K rows are padded to D+8 bf16, so
+// consecutive rows start 4 banks apart and the 16 lanes a ds_read_b128
+// serves per cycle cover all 64 banks; V rows are padded to D+32 bf16, so the
+// four rows a transposed read touches start 16 banks apart and its 32 lanes
+// per cycle (two 16-lane groups 8 banks apart) cover all 64 banks.
+//
+// Pipelining (the HEG pipe knob on the load/body boundary).  DBUF = 1: two
+// LDS slots; the global loads of tile t+1 are in flight while tile t is
+// computed, then written to the other slot; one barrier per tile.  DBUF = 0:
+// one slot, load -> barrier -> compute -> barrier; overlap then comes from
+// the other workgroups resident on the CU.  Only the tiles that hold the
+// ragged end of the key range or cross the workgroup's causal diagonal run
+// the masking code.
+//
+// The scale factor is strictly positive (the host maps a zero scale to the
+// smallest normal float, which gives exactly equal weights), so masked scores
+// of -inf always give a probability of exactly 0.
 #pragma once
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace attn {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+
+static constexpr bf16x2 kOnes2 = {(__bf16)1.0f, (__bf16)1.0f};
+// Slack (log2 units) before the running max of a row is moved.
+static constexpr float kRescaleSlack = 8.0f;
 
 template <int D, int BN>
 struct FwdLds {
-    static constexpr int K_STRIDE = D + 8;   // bf16 per K row (16-byte pad)
-    static constexpr int V_STRIDE = BN + 8;  // bf16 per V^T row (16-byte pad)
-    static constexpr int K_ELEMS = BN * K_STRIDE;
-    static constexpr int V_ELEMS = D * V_STRIDE;
-    static constexpr int SLOT = K_ELEMS + V_ELEMS;
+    static constexpr int K_STRIDE = D + 8;   // bf16 per K row
+    static constexpr int V_STRIDE = D + 32;  // bf16 per V row
+    static constexpr int K_TILE = BN * K_STRIDE;
+    static constexpr int V_TILE = BN * V_STRIDE;
 };
 
 // LDS row of key j (0..31) inside a 32-key block; inverse of the permutation
@@ -53,14 +79,28 @@ __device__ __forceinline__ int k_lds_row(int j) {
     return ((j >> 2) & 3) << 3 | (j >> 4) << 2 | (j & 3);
 }
 
-__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+__device__ __forceinline__ float half_swap_max(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
+                                                    false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__device__ __forceinline__ float half_swap_sum(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
+                                                    false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+__device__ __forceinline__ s16x4 lds_read_tr(const uint16_t* p) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) s16x4*)(p));
+}
 
 // Waves per SIMD the register allocator should leave room for: two when two
 // workgroups' LDS fits in one CU (or one 8-wave workgroup), else one.
 template <int D, int BN, int NW, bool DBUF>
 constexpr int fwd_waves_per_eu() {
-    constexpr int lds = (DBUF ? 2 : 1) * FwdLds<D, BN>::SLOT * 2;
+    constexpr int lds = (DBUF ? 2 : 1) * (FwdLds<D, BN>::K_TILE + FwdLds<D, BN>::V_TILE) * 2;
     constexpr int wgs = 163840 / lds;
     return (wgs * NW / 4) >= 2 ? 2 : 1;
 }
@@ -76,12 +116,15 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, DBUF>())) voi
     constexpr int KB = BN / 32;  // 32-key blocks per tile
     constexpr int CB = D / 32;   // 32-dim blocks of the output
     using L = FwdLds<D, BN>;
-    constexpr int K_CHUNKS = BN * D / 8;         // 16-byte chunks of a K tile
-    constexpr int V_GROUPS = (BN / 4) * (D / 8); // 4 keys x 8 dims groups of V
-    constexpr int KCH = (K_CHUNKS + NT - 1) / NT;
-    constexpr int VCH = (V_GROUPS + NT - 1) / NT;
+    constexpr int CHUNKS = BN * D / 8;  // 16-byte chunks of one K (or V) tile
+    constexpr int CH = (CHUNKS + NT - 1) / NT;
+    constexpr int NSLOT = DBUF ? 2 : 1;
 
-    __shared__ __attribute__((aligned(16))) uint16_t lds[(DBUF ? 2 : 1) * L::SLOT];
+    __shared__ __attribute__((aligned(16))) uint16_t lds[NSLOT * (L::K_TILE + L::V_TILE)];
+    uint16_t* const kslot0 = lds;
+    uint16_t* const kslot1 = lds + (DBUF ? L::K_TILE : 0);
+    uint16_t* const vslot0 = lds + NSLOT * L::K_TILE;
+    uint16_t* const vslot1 = vslot0 + (DBUF ? L::V_TILE : 0);
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -109,11 +152,11 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, DBUF>())) voi
     // ---- Q tile into VGPRs, as the B operand (16 dims x 32 queries) --------
     bf16x8 qf[KD];
     {
-        const uint16_t* qp = Q + ((long long)bh * Sq + qrow) * D + hh * 8;
+        // rows past Sq read the last row (finite data; never stored)
+        const uint16_t* qp = Q + ((long long)bh * Sq + min(qrow, Sq - 1)) * D + hh * 8;
 #pragma unroll
         for (int ks = 0; ks < KD; ++ks) {
-            u32x4 w = {0u, 0u, 0u, 0u};
-            if (qrow < Sq) w = *reinterpret_cast<const u32x4*>(qp + ks * 16);
+            u32x4 w = *reinterpret_cast<const u32x4*>(qp + ks * 16);
             w ^= q_sign;  // exact negation for a negative scale
             qf[ks] = __builtin_bit_cast(bf16x8, w);
         }
@@ -126,71 +169,46 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, DBUF>())) voi
         kv_end = min(Skv, last_q + diag + 1);
     }
     const int n_tiles = (kv_end + BN - 1) / BN;
+    // causal: a tile entirely above this wave's diagonal is skipped
+    auto wave_active = [&](int t) { return !CAUSAL || t * BN <= q_wave0 + 31 + diag; };
 
     const long long kv_base = (long long)bh * Skv * D;
     const uint16_t* Kb = K + kv_base;
     const uint16_t* Vb = V + kv_base;
 
-    u32x4 kreg[KCH];
-    u32x4 vreg[VCH][4];
-
-    auto load_tile = [&](int t) {
+    // Rows past the end of the key range are loaded from the last valid row
+    // (clamped, never out of bounds): their scores are masked to weight 0,
+    // and their V values are finite, so they contribute exactly 0.
+    auto load_rows = [&](const uint16_t* base, int t, u32x4 (&reg)[CH]) {
         const int key0 = t * BN;
 #pragma unroll
-        for (int i = 0; i < KCH; ++i) {
+        for (int i = 0; i < CH; ++i) {
             const int u = tid + i * NT;
-            kreg[i] = u32x4{0u, 0u, 0u, 0u};
-            if (u < K_CHUNKS) {
+            if (CHUNKS % NT == 0 || u < CHUNKS) {
                 const int j = u / (D / 8), cc = u % (D / 8);
-                if (key0 + j < Skv)
-                    kreg[i] = *reinterpret_cast<const u32x4*>(Kb + (long long)(key0 + j) * D + cc * 8);
-            }
-        }
-#pragma unroll
-        for (int i = 0; i < VCH; ++i) {
-            const int g = tid + i * NT;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) vreg[i][r] = u32x4{0u, 0u, 0u, 0u};
-            if (g < V_GROUPS) {
-                const int kq = g / (D / 8), cc = g % (D / 8);
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int key = key0 + 4 * kq + r;
-                    if (key < Skv)
-                        vreg[i][r] = *reinterpret_cast<const u32x4*>(Vb + (long long)key * D + cc * 8);
-                }
+                const int key = min(key0 + j, Skv - 1);
+                reg[i] = *reinterpret_cast<const u32x4*>(base + (long long)key * D + cc * 8);
             }
         }
     };
-
-    auto store_tile = [&](uint16_t* slot) {
-        uint16_t* kl = slot;
-        uint16_t* vl = slot + L::K_ELEMS;
+    auto store_k = [&](uint16_t* dst, const u32x4 (&reg)[CH]) {
 #pragma unroll
-        for (int i = 0; i < KCH; ++i) {
+        for (int i = 0; i < CH; ++i) {
             const int u = tid + i * NT;
-            if (u < K_CHUNKS) {
+            if (CHUNKS % NT == 0 || u < CHUNKS) {
                 const int j = u / (D / 8), cc = u % (D / 8);
                 const int prow = (j & ~31) | k_lds_row(j & 31);
-                *reinterpret_cast<u32x4*>(kl + prow * L::K_STRIDE + cc * 8) = kreg[i];
+                *reinterpret_cast<u32x4*>(dst + prow * L::K_STRIDE + cc * 8) = reg[i];
             }
         }
-        // V is written transposed: V^T[dim][key], 4 keys (8 bytes) per store.
+    };
+    auto store_v = [&](uint16_t* dst, const u32x4 (&reg)[CH]) {
 #pragma unroll
-        for (int i = 0; i < VCH; ++i) {
-            const int g = tid + i * NT;
-            if (g < V_GROUPS) {
-                const int kq = g / (D / 8), cc = g % (D / 8);
-#pragma unroll
-                for (int w = 0; w < 4; ++w) {
-                    const uint32_t a0 = vreg[i][0][w], a1 = vreg[i][1][w];
-                    const uint32_t a2 = vreg[i][2][w], a3 = vreg[i][3][w];
-                    u32x2 even = {(a0 & 0xffffu) | (a1 << 16), (a2 & 0xffffu) | (a3 << 16)};
-                    u32x2 odd = {(a0 >> 16) | (a1 & 0xffff0000u), (a2 >> 16) | (a3 & 0xffff0000u)};
-                    const int c = cc * 8 + 2 * w;
-                    *reinterpret_cast<u32x2*>(vl + c * L::V_STRIDE + 4 * kq) = even;
-                    *reinterpret_cast<u32x2*>(vl + (c + 1) * L::V_STRIDE + 4 * kq) = odd;
-                }
+        for (int i = 0; i < CH; ++i) {
+            const int u = tid + i * NT;
+            if (CHUNKS % NT == 0 || u < CHUNKS) {
+                const int j = u / (D / 8), cc = u % (D / 8);
+                *reinterpret_cast<u32x4*>(dst + j * L::V_STRIDE + cc * 8) = reg[i];
             }
         }
     };
@@ -204,122 +222,162 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, DBUF>())) voi
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[cb][r] = 0.f;
 
-    auto compute_tile = [&](const uint16_t* slot, int t) {
-        const int key0 = t * BN;
-        // whole tile above this wave's diagonal: nothing to do
-        if (CAUSAL && key0 > q_wave0 + 31 + diag) return;
-        const uint16_t* kl = slot;
-        const uint16_t* vl = slot + L::K_ELEMS;
-
-        // S^T = K Q^T
-        f32x16 s[KB];
+    // S^T = K Q^T for one tile (independent accumulators interleaved)
+    auto scores = [&](const uint16_t* kl, f32x16 (&s)[KB]) {
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb) {
+        for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
             for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
-            const uint16_t* ka = kl + (kb * 32 + l32) * L::K_STRIDE + hh * 8;
 #pragma unroll
-            for (int ks = 0; ks < KD; ++ks) {
-                const bf16x8 a = *reinterpret_cast<const bf16x8*>(ka + ks * 16);
+        for (int ks = 0; ks < KD; ++ks)
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb) {
+                const bf16x8 a = *reinterpret_cast<const bf16x8*>(
+                    kl + (kb * 32 + l32) * L::K_STRIDE + hh * 8 + ks * 16);
                 s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], s[kb], 0, 0, 0);
             }
-        }
+    };
 
-        // mask: ragged tail of the key range and, on diagonal tiles, causality
-        const bool need_mask = (key0 + BN > Skv) || (CAUSAL && key0 + BN - 1 > q_wave0 + diag);
-        const int lim = CAUSAL ? min(Skv - 1, qrow + diag) : Skv - 1;
-        if (need_mask) {
+    // Online-softmax statistics of tile t: mask (MASK tiles only), row max,
+    // and the lazy rescale.  The running max m_i of a row only moves when the
+    // tile's max exceeds it by more than kRescaleSlack (log2 units), so the
+    // output rescale is skipped on almost every tile; probabilities are then
+    // bounded by 2^kRescaleSlack, and the numerator and the normaliser share
+    // the same reference, so the result is unchanged.  Returns the reference
+    // to subtract.
+    auto softmax_stats = [&](f32x16 (&s)[KB], int t, auto mask_tag) -> float {
+        constexpr bool MASK = decltype(mask_tag)::value;
+        const int key0 = t * BN;
+        if (MASK) {
+            // ragged tail of the key range and, on diagonal tiles, causality
+            const int lim = CAUSAL ? min(Skv - 1, qrow + diag) : Skv - 1;
 #pragma unroll
             for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int key = key0 + kb * 32 + 16 * hh + r;
-                    if (key > lim) s[kb][r] = -INFINITY;
-                }
+                for (int r = 0; r < 16; ++r)
+                    if (key0 + kb * 32 + 16 * hh + r > lim) s[kb][r] = -INFINITY;
         }
-
-        // row max over this tile (in-lane, then across the two wave halves)
         float mx = -INFINITY;
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
             for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        // (a fully masked row gives -inf, also when the scale is 0)
+        mx = half_swap_max(mx);
         const float tmax = (mx == -INFINITY) ? -INFINITY : mx * scale_log2;
-        const float m_new = fmaxf(m_i, tmax);
-        const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-        const float alpha = __builtin_amdgcn_exp2f(m_i - m_use);
+        const bool move = tmax > m_i + kRescaleSlack;  // also true for the first finite max
+        if (__any(move)) {
+            const float m_new = move ? tmax : m_i;
+            const float alpha = __builtin_amdgcn_exp2f(m_i - m_new);  // 0 when m_i = -inf
+            l_i *= alpha;
+#pragma unroll
+            for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) oacc[cb][r] *= alpha;
+            m_i = m_new;
+        }
+        return (m_i == -INFINITY) ? 0.f : m_i;
+    };
 
-        // probabilities, rounded to bf16 (RNE), and their sum
-        bf16x8 pb[KB][2];
+    // bf16 probabilities of tile t and their sum (branch-free).  Masked
+    // scores are -inf and the scale is > 0, so they give exactly 0.
+    auto softmax_exp = [&](const f32x16 (&s)[KB], float m_use, bf16x8 (&pb)[KB][2]) {
         float rs = 0.f;
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
             for (int h2 = 0; h2 < 2; ++h2) {
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    float p = __builtin_amdgcn_exp2f(fmaf(s[kb][8 * h2 + e], scale_log2, -m_use));
-                    // masked keys weigh exactly 0 (their score is -inf, and -inf * 0 = NaN)
-                    if (need_mask && key0 + kb * 32 + 16 * hh + 8 * h2 + e > lim) p = 0.f;
-                    pb[kb][h2][e] = (__bf16)p;
-                }
-                const u32x4 w = __builtin_bit_cast(u32x4, pb[kb][h2]);
+                for (int e = 0; e < 8; ++e)
+                    pb[kb][h2][e] =
+                        (__bf16)__builtin_amdgcn_exp2f(fmaf(s[kb][8 * h2 + e], scale_log2, -m_use));
+                // sum of the rounded probabilities, two per v_dot2c_f32_bf16
 #pragma unroll
-                for (int e = 0; e < 4; ++e) rs += bf16_lo(w[e]) + bf16_hi(w[e]);
+                for (int e = 0; e < 4; ++e) {
+                    const bf16x2 pair = {pb[kb][h2][2 * e], pb[kb][h2][2 * e + 1]};
+                    rs = __builtin_amdgcn_fdot2_f32_bf16(pair, kOnes2, rs, false);
+                }
             }
-        l_i = l_i * alpha + rs;
+        l_i += rs;
+    };
 
-        // rescale the output only when some row's max moved
-        if (__any(m_new > m_i)) {
+    // O^T += V^T P^T; V^T operands by transposed LDS reads
+    const int tr_row = (lane & 15) >> 2;                         // + k0
+    const int tr_col = ((lane >> 4) & 1) * 16 + 4 * (lane & 3);  // + cb*32
+    auto pv = [&](const uint16_t* vl, const bf16x8 (&pb)[KB][2]) {
 #pragma unroll
-            for (int cb = 0; cb < CB; ++cb)
+        for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-                for (int r = 0; r < 16; ++r) oacc[cb][r] *= alpha;
-        }
-        m_i = m_new;
-
-        // O^T += V^T P^T
+            for (int h2 = 0; h2 < 2; ++h2)
 #pragma unroll
-        for (int cb = 0; cb < CB; ++cb) {
-            const uint16_t* va = vl + (cb * 32 + l32) * L::V_STRIDE + 16 * hh;
-#pragma unroll
-            for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-                for (int h2 = 0; h2 < 2; ++h2) {
-                    const bf16x8 a = *reinterpret_cast<const bf16x8*>(va + kb * 32 + 8 * h2);
-                    oacc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kb][h2], oacc[cb], 0, 0, 0);
+                for (int cb = 0; cb < CB; ++cb) {
+                    const uint16_t* p =
+                        vl + (kb * 32 + 16 * hh + 8 * h2 + tr_row) * L::V_STRIDE + cb * 32 + tr_col;
+                    const s16x4 lo = lds_read_tr(p);
+                    const s16x4 hi = lds_read_tr(p + 4 * L::V_STRIDE);
+                    const s16x8 w = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+                    oacc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        __builtin_bit_cast(bf16x8, w), pb[kb][h2], oacc[cb], 0, 0, 0);
                 }
-        }
+    };
+
+    // Tiles before first_masked need no mask for any row of this workgroup.
+    int first_masked = Skv / BN;  // the ragged tail tile, if any
+    if (CAUSAL) first_masked = min(first_masked, (qt * BM + diag + 1) / BN);
+    first_masked = min(first_masked, n_tiles);
+
+    auto compute = [&](const uint16_t* kl, const uint16_t* vl, int t, auto mask_tag) {
+        if (!wave_active(t)) return;
+        f32x16 s[KB];
+        bf16x8 pb[KB][2];
+        scores(kl, s);
+        const float m_ref = softmax_stats(s, t, mask_tag);
+        softmax_exp(s, m_ref, pb);
+        pv(vl, pb);
     };
 
     // ---- main loop over K/V tiles ------------------------------------------
-    uint16_t* slot0 = lds;
-    uint16_t* slot1 = lds + (DBUF ? L::SLOT : 0);
-    load_tile(0);
-    store_tile(slot0);
-    __syncthreads();
-    for (int t = 0; t < n_tiles; ++t) {
-        uint16_t* cur = (DBUF && (t & 1)) ? slot1 : slot0;
-        if (DBUF && t + 1 < n_tiles) load_tile(t + 1);
-        compute_tile(cur, t);
-        if (t + 1 < n_tiles) {
-            if (DBUF) {
-                store_tile((t & 1) ? slot0 : slot1);
-                __syncthreads();
-            } else {
-                __syncthreads();
-                load_tile(t + 1);
-                store_tile(slot0);
-                __syncthreads();
+    u32x4 kr[CH], vr[CH];
+    if (DBUF) {
+        // tile t+1 is fetched into registers while tile t is computed from
+        // LDS, then written to the other slot; one barrier per tile
+        load_rows(Kb, 0, kr);
+        load_rows(Vb, 0, vr);
+        store_k(kslot0, kr);
+        store_v(vslot0, vr);
+        __syncthreads();
+        auto step = [&](int t, auto mask_tag) {
+            const bool odd = t & 1;
+            if (t + 1 < n_tiles) {
+                load_rows(Kb, t + 1, kr);
+                load_rows(Vb, t + 1, vr);
             }
-        }
+            compute(odd ? kslot1 : kslot0, odd ? vslot1 : vslot0, t, mask_tag);
+            if (t + 1 < n_tiles) {
+                store_k(odd ? kslot0 : kslot1, kr);
+                store_v(odd ? vslot0 : vslot1, vr);
+            }
+            __syncthreads();
+        };
+        int t = 0;
+        for (; t < first_masked; ++t) step(t, std::false_type{});
+        for (; t < n_tiles; ++t) step(t, std::true_type{});
+    } else {
+        auto step = [&](int t, auto mask_tag) {
+            load_rows(Kb, t, kr);
+            load_rows(Vb, t, vr);
+            store_k(kslot0, kr);
+            store_v(vslot0, vr);
+            __syncthreads();
+            compute(kslot0, vslot0, t, mask_tag);
+            __syncthreads();
+        };
+        int t = 0;
+        for (; t < first_masked; ++t) step(t, std::false_type{});
+        for (; t < n_tiles; ++t) step(t, std::true_type{});
     }
 
     // ---- epilogue: O = O^T / l, one query row per lane ----------------------
-    const float l_tot = l_i + __shfl_xor(l_i, 32);
-    const float inv = 1.f / l_tot;
+    const float inv = 1.f / half_swap_sum(l_i);
     if (qrow < Sq) {
         float* orow = O + ((long long)bh * Sq + qrow) * D + 4 * hh;
 #pragma unroll

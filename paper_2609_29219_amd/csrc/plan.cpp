@@ -72,21 +72,22 @@ struct FwdCost {
     const char* bound;
 };
 
-// VGPRs per lane of one prefill wave (Q operand, score and output
-// accumulators, bf16 probabilities, prefetch registers, scalars/addresses).
+// VGPRs per lane of one prefill wave: Q operand (d/4), score accumulators
+// (bn/2; a second set while the next tile's scores overlap the softmax),
+// bf16 probabilities (bn/4), output accumulator (d/2), staging registers of
+// the K and V tiles, and scalars/addresses.
 int fwd_vgprs(int d, int bn, int waves, int dbuf) {
     const int nt = waves * 64;
-    const int kch = (bn * d / 8 + nt - 1) / nt;
-    const int vch = ((bn / 4) * (d / 8) + nt - 1) / nt;
-    const int prefetch = kch * 4 + vch * 16;
-    int v = d / 4 + bn / 2 + d / 2 + bn / 4 + (dbuf ? prefetch : prefetch / 2) + 24;
+    const int ch = (bn * d / 8 + nt - 1) / nt;
+    const int scores = dbuf ? bn : bn / 2;
+    int v = d / 4 + scores + bn / 4 + d / 2 + 2 * ch * 4 + 24;
     return round_up(v, 8);
 }
 
 }  // namespace
 
 bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d,
-                    int causal, int bn, int waves, int dbuf, FwdPlan* out) {
+                    int causal, int bn, int waves, int dbuf, FwdPlan* out, FwdResFn res) {
     FwdPlan p;
     p.d = d;
     p.block_n = bn;
@@ -106,6 +107,13 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
     int wg = desc.lds_bytes_per_cu / p.lds_bytes;
     wg = std::min(wg, (wpe_regs * simds) / waves);
     wg = std::min(wg, (desc.max_waves_per_simd * simds) / waves);
+    if (res) {  // the compiled kernel's real footprint overrides the estimate
+        KernelRes kr;
+        if (!res(d, bn, waves, dbuf, causal, &kr)) return false;
+        if (kr.scratch_bytes > 0) return false;  // spills: not a valid primitive
+        wg = kr.wg_per_cu;
+        if (kr.vgprs > 0) p.vgprs = kr.vgprs;
+    }
     if (wg < 1) return false;
     p.wg_per_cu = wg;
     p.n_qtiles = (Sq + p.block_m - 1) / p.block_m;
@@ -181,14 +189,15 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
 }
 
 bool plan_fwd(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d, int causal,
-              FwdPlan* out) {
+              FwdPlan* out, FwdResFn res) {
     bool found = false;
     FwdPlan best;
     for (int bn : kFwdBlockN)
         for (int waves : kFwdWaves)
             for (int dbuf : kFwdDbuf) {
                 FwdPlan p;
-                if (!plan_fwd_fixed(desc, B, H, Sq, Skv, d, causal, bn, waves, dbuf, &p)) continue;
+                if (!plan_fwd_fixed(desc, B, H, Sq, Skv, d, causal, bn, waves, dbuf, &p, res))
+                    continue;
                 // strict improvement keeps the first (smallest) candidate on ties
                 if (!found || p.modeled_us < best.modeled_us * (1.0 - 1e-9)) {
                     best = p;
