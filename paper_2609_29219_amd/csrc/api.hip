@@ -21,18 +21,18 @@ hipError_t launch_fwd_d64(const FwdPlan&, const void*, const void*, const void*,
 hipError_t launch_fwd_d128(const FwdPlan&, const void*, const void*, const void*, float*, int,
                            int, float, uint32_t, int, hipStream_t);
 
-bool fwd_resources_d64(int bn, int waves, int dbuf, int causal, KernelRes* r);
-bool fwd_resources_d128(int bn, int waves, int dbuf, int causal, KernelRes* r);
+bool fwd_resources_d64(int bn, int waves, int pipe, int causal, KernelRes* r);
+bool fwd_resources_d128(int bn, int waves, int pipe, int causal, KernelRes* r);
 
-bool fwd_resources(int d, int bn, int waves, int dbuf, int causal, KernelRes* r) {
-    if (d == 64) return fwd_resources_d64(bn, waves, dbuf, causal, r);
-    if (d == 128) return fwd_resources_d128(bn, waves, dbuf, causal, r);
+bool fwd_resources(int d, int bn, int waves, int pipe, int causal, KernelRes* r) {
+    if (d == 64) return fwd_resources_d64(bn, waves, pipe, causal, r);
+    if (d == 128) return fwd_resources_d128(bn, waves, pipe, causal, r);
     return false;
 }
 
 // Forced tiles (ablation only) may run a variant that spills: slow, not wrong.
-bool fwd_resources_forced(int d, int bn, int waves, int dbuf, int causal, KernelRes* r) {
-    if (!fwd_resources(d, bn, waves, dbuf, causal, r)) return false;
+bool fwd_resources_forced(int d, int bn, int waves, int pipe, int causal, KernelRes* r) {
+    if (!fwd_resources(d, bn, waves, pipe, causal, r)) return false;
     r->scratch_bytes = 0;
     return true;
 }
@@ -129,11 +129,11 @@ int device_state(DeviceState** out) {
 }
 
 // Optional fixed tile choice for the block-size ablation only:
-// ATTN_FORCE_PLAN="bn=64,waves=4,dbuf=1".  Never used to select tiles.
-bool forced_fwd(int* bn, int* waves, int* dbuf) {
+// ATTN_FORCE_PLAN="bn=64,waves=8,pipe=2".  Never used to select tiles.
+bool forced_fwd(int* bn, int* waves, int* pipe) {
     const char* s = getenv("ATTN_FORCE_PLAN");
     if (!s || !*s) return false;
-    return sscanf(s, "bn=%d,waves=%d,dbuf=%d", bn, waves, dbuf) == 3;
+    return sscanf(s, "bn=%d,waves=%d,pipe=%d", bn, waves, pipe) == 3;
 }
 
 int validate_common(const void* q, const void* k, const void* v, const void* o, int B, int H,
@@ -241,9 +241,9 @@ int attn_fwd(const void* q, const void* k, const void* v, float* o, int B, int H
 
     const int c = causal ? 1 : 0;
     FwdPlan plan;
-    int fbn, fw, fdb;
-    if (forced_fwd(&fbn, &fw, &fdb)) {
-        if (!plan_fwd_fixed(st->desc, B, H, Sq, Skv, d, c, fbn, fw, fdb, &plan,
+    int fbn, fw, fpipe;
+    if (forced_fwd(&fbn, &fw, &fpipe)) {
+        if (!plan_fwd_fixed(st->desc, B, H, Sq, Skv, d, c, fbn, fw, fpipe, &plan,
                             fwd_resources_forced))
             return fail(ATTN_EINVAL, "ATTN_FORCE_PLAN names an infeasible or unknown tile");
     } else {

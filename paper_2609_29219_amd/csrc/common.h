@@ -15,7 +15,7 @@ struct FwdPlan {
     int block_m = 0;    // queries per workgroup (32 per wave)
     int block_n = 0;    // keys per K/V tile staged in LDS
     int waves = 0;      // waves per workgroup
-    int dbuf = 0;       // 1: two LDS slots, next tile prefetched during compute
+    int pipe = 0;       // 0 serial, 1 next tile prefetched, 2 ping-pong wave groups
     int causal = 0;
     int lds_bytes = 0;  // per workgroup
     int vgprs = 0;      // modelled VGPRs per lane
@@ -42,14 +42,14 @@ struct DecodePlan {
 // Candidate domains: every point is an instantiated kernel.
 constexpr int kFwdBlockN[] = {32, 64, 128};
 constexpr int kFwdWaves[] = {4, 8};
-constexpr int kFwdDbuf[] = {0, 1};
+constexpr int kFwdPipe[] = {0, 1, 2};  // 2 only with 8 waves
 constexpr int kDecodeThreads = 256;
 constexpr int kDecodeUnroll = 8;
 
 // LDS footprint of a prefill workgroup: K tile [BN][D+8] and V tile
-// [BN][D+16] in bf16, times two slots when double buffered.
-constexpr int fwd_lds_bytes(int d, int bn, int dbuf) {
-    return (dbuf ? 2 : 1) * (bn * (d + 8) + bn * (d + 32)) * 2;
+// [BN][D+32] in bf16, one slot each (pipe 0) or two (pipe 1, 2).
+constexpr int fwd_lds_bytes(int d, int bn, int pipe) {
+    return (pipe == 0 ? 1 : 2) * (bn * (d + 8) + bn * (d + 32)) * 2;
 }
 
 // Resource usage of one compiled prefill variant, as the runtime reports it:
@@ -60,7 +60,7 @@ struct KernelRes {
     int scratch_bytes = 0;
     int vgprs = 0;
 };
-typedef bool (*FwdResFn)(int d, int bn, int waves, int dbuf, int causal, KernelRes* out);
+typedef bool (*FwdResFn)(int d, int bn, int waves, int pipe, int causal, KernelRes* out);
 
 // Planner (host only, pure arithmetic on the device description).  With
 // res == nullptr (no device) the register footprint is estimated.
@@ -68,9 +68,9 @@ void default_desc(attn_device_desc* out);
 bool plan_fwd(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d, int causal,
               FwdPlan* out, FwdResFn res = nullptr);
 bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d,
-                    int causal, int bn, int waves, int dbuf, FwdPlan* out,
+                    int causal, int bn, int waves, int pipe, FwdPlan* out,
                     FwdResFn res = nullptr);
-bool fwd_resources(int d, int bn, int waves, int dbuf, int causal, KernelRes* out);
+bool fwd_resources(int d, int bn, int waves, int pipe, int causal, KernelRes* out);
 bool plan_decode(const attn_device_desc& desc, int B, int H, int Skv, int d, int n_splits,
                  DecodePlan* out);
 int format_fwd_plan(const FwdPlan& p, char* buf, int buflen);

@@ -19,10 +19,10 @@
 // consecutive keys, which is the k-operand layout the PV MFMA needs.
 //
 // PV.  O^T += V^T P^T with B = the bf16 probabilities straight from
-// registers and A = V^T (32 dims x 16 keys).  V stays row-major in LDS and
-// the A operand is fetched with ds_read_b64_tr_b16: inside each 16-lane
-// group, lane i addresses 4 consecutive values E[i][0..3] and lane 4a+b
-// receives E[a][b], E[a+4][b], E[a+8][b], E[a+12][b].  Lane i points at
+// registers and A = V^T (32 dims x 8 keys per MFMA).  V stays row-major in
+// LDS and the A operand is fetched with ds_read_b64_tr_b16: inside each
+// 16-lane group, lane i addresses 4 consecutive values E[i][0..3] and lane
+// 4a+b receives E[a][b], E[a+4][b], E[a+8][b], E[a+12][b].  Lane i points at
 // row k0 + i/4, column base + 4*(i%4), so lane j receives the 4 keys
 // k0..k0+3 of column base + j; two such reads give the 8 keys of one MFMA.
 // The output accumulator holds one query per lane, so the online-softmax
@@ -34,13 +34,19 @@
 // four rows a transposed read touches start 16 banks apart and its 32 lanes
 // per cycle (two 16-lane groups 8 banks apart) cover all 64 banks.
 //
-// Pipelining (the HEG pipe knob on the load/body boundary).  DBUF = 1: two
-// LDS slots; the global loads of tile t+1 are in flight while tile t is
-// computed, then written to the other slot; one barrier per tile.  DBUF = 0:
-// one slot, load -> barrier -> compute -> barrier; overlap then comes from
-// the other workgroups resident on the CU.  Only the tiles that hold the
-// ragged end of the key range or cross the workgroup's causal diagonal run
-// the masking code.
+// Pipelining (the HEG pipe knob, PIPE):
+//   0  one LDS slot per operand: load -> barrier -> compute -> barrier; any
+//      overlap comes from the other workgroups resident on the CU.
+//   1  two slots: the global loads of tile t+1 are in flight while tile t is
+//      computed, then written to the other slot; one barrier per tile.
+//   2  ping-pong (8 waves): a wave cannot issue vector instructions while its
+//      own MFMAs execute, but the two waves sharing a SIMD can.  Waves 0-3
+//      (group A) and 4-7 (group B, one of each per SIMD) therefore run in
+//      opposite phases: while A issues the MFMAs of PV(t-1) and S(t), B runs
+//      the softmax of tile t on the VALU, and the other way round in the
+//      second half of the tile; two barriers per tile.
+// Only the tiles that hold the ragged end of the key range or cross the
+// workgroup's causal diagonal run the masking code.
 //
 // The scale factor is strictly positive (the host maps a zero scale to the
 // smallest normal float, which gives exactly equal weights), so masked scores
@@ -61,7 +67,6 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x8 __attribute__((ext_vector_type(8)));
 
-static constexpr bf16x2 kOnes2 = {(__bf16)1.0f, (__bf16)1.0f};
 // Slack (log2 units) before the running max of a row is moved.
 static constexpr float kRescaleSlack = 8.0f;
 
@@ -96,20 +101,23 @@ __device__ __forceinline__ s16x4 lds_read_tr(const uint16_t* p) {
         (__attribute__((address_space(3))) s16x4*)(p));
 }
 
+constexpr int fwd_slots(int pipe) { return pipe == 0 ? 1 : 2; }
+
 // Waves per SIMD the register allocator should leave room for: two when two
 // workgroups' LDS fits in one CU (or one 8-wave workgroup), else one.
-template <int D, int BN, int NW, bool DBUF>
+template <int D, int BN, int NW, int PIPE>
 constexpr int fwd_waves_per_eu() {
-    constexpr int lds = (DBUF ? 2 : 1) * (FwdLds<D, BN>::K_TILE + FwdLds<D, BN>::V_TILE) * 2;
+    constexpr int lds = fwd_slots(PIPE) * (FwdLds<D, BN>::K_TILE + FwdLds<D, BN>::V_TILE) * 2;
     constexpr int wgs = 163840 / lds;
     return (wgs * NW / 4) >= 2 ? 2 : 1;
 }
 
-template <int D, int BN, int NW, bool DBUF, bool CAUSAL>
-__global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, DBUF>())) void fwd_kernel(
+template <int D, int BN, int NW, int PIPE, bool CAUSAL>
+__global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) void fwd_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, float* __restrict__ O, int Sq, int Skv, int n_qtiles,
     int n_wg, int num_xcds, float scale_log2, uint32_t q_sign) {
+    static_assert(PIPE != 2 || NW == 8, "the ping-pong schedule pairs 4 waves with 4 waves");
     constexpr int BM = NW * 32;
     constexpr int NT = NW * 64;
     constexpr int KD = D / 16;   // MFMA k-steps over the head dimension
@@ -118,13 +126,13 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, DBUF>())) voi
     using L = FwdLds<D, BN>;
     constexpr int CHUNKS = BN * D / 8;  // 16-byte chunks of one K (or V) tile
     constexpr int CH = (CHUNKS + NT - 1) / NT;
-    constexpr int NSLOT = DBUF ? 2 : 1;
+    constexpr int NSLOT = fwd_slots(PIPE);
 
     __shared__ __attribute__((aligned(16))) uint16_t lds[NSLOT * (L::K_TILE + L::V_TILE)];
     uint16_t* const kslot0 = lds;
-    uint16_t* const kslot1 = lds + (DBUF ? L::K_TILE : 0);
+    uint16_t* const kslot1 = lds + (NSLOT - 1) * L::K_TILE;
     uint16_t* const vslot0 = lds + NSLOT * L::K_TILE;
-    uint16_t* const vslot1 = vslot0 + (DBUF ? L::V_TILE : 0);
+    uint16_t* const vslot1 = vslot0 + (NSLOT - 1) * L::V_TILE;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -171,6 +179,9 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, DBUF>())) voi
     const int n_tiles = (kv_end + BN - 1) / BN;
     // causal: a tile entirely above this wave's diagonal is skipped
     auto wave_active = [&](int t) { return !CAUSAL || t * BN <= q_wave0 + 31 + diag; };
+    // tiles before first_masked need no mask for any row of this workgroup
+    int first_masked = Skv / BN;  // the ragged tail tile, if any
+    if (CAUSAL) first_masked = min(first_masked, (qt * BM + diag + 1) / BN);
 
     const long long kv_base = (long long)bh * Skv * D;
     const uint16_t* Kb = K + kv_base;
@@ -222,8 +233,9 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, DBUF>())) voi
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[cb][r] = 0.f;
 
-    // S^T = K Q^T for one tile (independent accumulators interleaved)
+    // S^T = K Q^T for one tile (independent accumulators interleaved).
     auto scores = [&](const uint16_t* kl, f32x16 (&s)[KB]) {
+        const uint16_t* ka_base = kl + l32 * L::K_STRIDE + hh * 8;
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
@@ -232,8 +244,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, DBUF>())) voi
         for (int ks = 0; ks < KD; ++ks)
 #pragma unroll
             for (int kb = 0; kb < KB; ++kb) {
-                const bf16x8 a = *reinterpret_cast<const bf16x8*>(
-                    kl + (kb * 32 + l32) * L::K_STRIDE + hh * 8 + ks * 16);
+                const bf16x8 a = *reinterpret_cast<const bf16x8*>(ka_base + kb * 32 * L::K_STRIDE + ks * 16);
                 s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], s[kb], 0, 0, 0);
             }
     };
@@ -249,13 +260,16 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, DBUF>())) voi
         constexpr bool MASK = decltype(mask_tag)::value;
         const int key0 = t * BN;
         if (MASK) {
-            // ragged tail of the key range and, on diagonal tiles, causality
+            // ragged tail of the key range and, on diagonal tiles, causality:
+            // register r of block kb holds key key0 + 16*hh + (kb*32 + r), so
+            // compare the constant kb*32 + r against one per-lane bound
             const int lim = CAUSAL ? min(Skv - 1, qrow + diag) : Skv - 1;
+            const int room = lim - key0 - 16 * hh;
 #pragma unroll
             for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
                 for (int r = 0; r < 16; ++r)
-                    if (key0 + kb * 32 + 16 * hh + r > lim) s[kb][r] = -INFINITY;
+                    if (kb * 32 + r > room) s[kb][r] = -INFINITY;
         }
         float mx = -INFINITY;
 #pragma unroll
@@ -277,10 +291,9 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, DBUF>())) voi
         }
         return (m_i == -INFINITY) ? 0.f : m_i;
     };
-
-    // bf16 probabilities of tile t and their sum (branch-free).  Masked
-    // scores are -inf and the scale is > 0, so they give exactly 0.
-    auto softmax_exp = [&](const f32x16 (&s)[KB], float m_use, bf16x8 (&pb)[KB][2]) {
+    // bf16 probabilities of a tile and their sum (VALU only).  Masked scores
+    // are -inf and the scale is > 0, so they give exactly 0.
+    auto probs = [&](const f32x16 (&s)[KB], float m_ref, bf16x8 (&pb)[KB][2]) {
         float rs = 0.f;
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb)
@@ -289,55 +302,67 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, DBUF>())) voi
 #pragma unroll
                 for (int e = 0; e < 8; ++e)
                     pb[kb][h2][e] =
-                        (__bf16)__builtin_amdgcn_exp2f(fmaf(s[kb][8 * h2 + e], scale_log2, -m_use));
-                // sum of the rounded probabilities, two per v_dot2c_f32_bf16
+                        (__bf16)__builtin_amdgcn_exp2f(fmaf(s[kb][8 * h2 + e], scale_log2, -m_ref));
+                // sum of the rounded probabilities (bf16 -> fp32 is a shift or a
+                // mask); plain adds co-issue with another wave's MFMAs, which the
+                // bf16 dot-product instructions do not
+                const u32x4 w = __builtin_bit_cast(u32x4, pb[kb][h2]);
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const bf16x2 pair = {pb[kb][h2][2 * e], pb[kb][h2][2 * e + 1]};
-                    rs = __builtin_amdgcn_fdot2_f32_bf16(pair, kOnes2, rs, false);
-                }
+                for (int e = 0; e < 4; ++e)
+                    rs += __uint_as_float(w[e] << 16) + __uint_as_float(w[e] & 0xffff0000u);
             }
         l_i += rs;
     };
 
-    // O^T += V^T P^T; V^T operands by transposed LDS reads
+    // O^T += V^T P^T in groups of 8 keys; V^T operands by transposed reads.
     const int tr_row = (lane & 15) >> 2;                         // + k0
     const int tr_col = ((lane >> 4) & 1) * 16 + 4 * (lane & 3);  // + cb*32
     auto pv = [&](const uint16_t* vl, const bf16x8 (&pb)[KB][2]) {
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-            for (int h2 = 0; h2 < 2; ++h2)
+            for (int h2 = 0; h2 < 2; ++h2) {
+                const uint16_t* p =
+                    vl + (kb * 32 + 16 * hh + 8 * h2 + tr_row) * L::V_STRIDE + tr_col;
 #pragma unroll
                 for (int cb = 0; cb < CB; ++cb) {
-                    const uint16_t* p =
-                        vl + (kb * 32 + 16 * hh + 8 * h2 + tr_row) * L::V_STRIDE + cb * 32 + tr_col;
-                    const s16x4 lo = lds_read_tr(p);
-                    const s16x4 hi = lds_read_tr(p + 4 * L::V_STRIDE);
+                    const s16x4 lo = lds_read_tr(p + cb * 32);
+                    const s16x4 hi = lds_read_tr(p + cb * 32 + 4 * L::V_STRIDE);
                     const s16x8 w = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
                     oacc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                         __builtin_bit_cast(bf16x8, w), pb[kb][h2], oacc[cb], 0, 0, 0);
                 }
-    };
-
-    // Tiles before first_masked need no mask for any row of this workgroup.
-    int first_masked = Skv / BN;  // the ragged tail tile, if any
-    if (CAUSAL) first_masked = min(first_masked, (qt * BM + diag + 1) / BN);
-    first_masked = min(first_masked, n_tiles);
-
-    auto compute = [&](const uint16_t* kl, const uint16_t* vl, int t, auto mask_tag) {
-        if (!wave_active(t)) return;
-        f32x16 s[KB];
-        bf16x8 pb[KB][2];
-        scores(kl, s);
-        const float m_ref = softmax_stats(s, t, mask_tag);
-        softmax_exp(s, m_ref, pb);
-        pv(vl, pb);
+            }
     };
 
     // ---- main loop over K/V tiles ------------------------------------------
+    // Every schedule runs its tiles in two loops: first the tiles that need no
+    // mask, then the masked ones (compile-time tag), so the masking code never
+    // sits in the common loop body.
+    auto two_loops = [&](int t0, auto&& step) {
+        int t = t0;
+        const int split = max(t0, min(first_masked, n_tiles));
+        for (; t < split; ++t) step(t, std::false_type{});
+        for (; t < n_tiles; ++t) step(t, std::true_type{});
+    };
     u32x4 kr[CH], vr[CH];
-    if (DBUF) {
+    if (PIPE == 0) {
+        two_loops(0, [&](int t, auto mask_tag) {
+            load_rows(Kb, t, kr);
+            load_rows(Vb, t, vr);
+            store_k(kslot0, kr);
+            store_v(vslot0, vr);
+            __syncthreads();
+            if (wave_active(t)) {
+                f32x16 s[KB];
+                bf16x8 pb[KB][2];
+                scores(kslot0, s);
+                probs(s, softmax_stats(s, t, mask_tag), pb);
+                pv(vslot0, pb);
+            }
+            __syncthreads();
+        });
+    } else if (PIPE == 1) {
         // tile t+1 is fetched into registers while tile t is computed from
         // LDS, then written to the other slot; one barrier per tile
         load_rows(Kb, 0, kr);
@@ -345,35 +370,79 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, DBUF>())) voi
         store_k(kslot0, kr);
         store_v(vslot0, vr);
         __syncthreads();
-        auto step = [&](int t, auto mask_tag) {
+        two_loops(0, [&](int t, auto mask_tag) {
             const bool odd = t & 1;
             if (t + 1 < n_tiles) {
                 load_rows(Kb, t + 1, kr);
                 load_rows(Vb, t + 1, vr);
             }
-            compute(odd ? kslot1 : kslot0, odd ? vslot1 : vslot0, t, mask_tag);
+            if (wave_active(t)) {
+                f32x16 s[KB];
+                bf16x8 pb[KB][2];
+                scores(odd ? kslot1 : kslot0, s);
+                probs(s, softmax_stats(s, t, mask_tag), pb);
+                pv(odd ? vslot1 : vslot0, pb);
+            }
             if (t + 1 < n_tiles) {
                 store_k(odd ? kslot0 : kslot1, kr);
                 store_v(odd ? vslot0 : vslot1, vr);
             }
             __syncthreads();
-        };
-        int t = 0;
-        for (; t < first_masked; ++t) step(t, std::false_type{});
-        for (; t < n_tiles; ++t) step(t, std::true_type{});
+        });
     } else {
-        auto step = [&](int t, auto mask_tag) {
-            load_rows(Kb, t, kr);
-            load_rows(Vb, t, vr);
-            store_k(kslot0, kr);
-            store_v(vslot0, vr);
+        // Ping-pong.  LDS holds K_t, K_{t+1} and V_{t-1}, V_t in two-slot
+        // rings (tile t in slot t&1).  Per tile t:
+        //   phase 1: A: PV(t-1), S(t)          B: softmax(t)
+        //   phase 2: A: softmax(t)             B: PV(t), S(t+1)
+        // The global loads of K_{t+2} and V_{t+1} are issued at the start of
+        // phase 1 and written to LDS at the end of phase 2 (into the slots of
+        // K_t and V_{t-1}, whose last readers finished in phase 1).
+        const bool group_b = wave >= 4;
+        f32x16 s[KB];
+        bf16x8 pb[KB][2];
+        bool pv_pending = false;  // group A: PV of the previous tile is due
+        load_rows(Kb, 0, kr);
+        load_rows(Vb, 0, vr);
+        store_k(kslot0, kr);
+        store_v(vslot0, vr);
+        if (n_tiles > 1) {
+            load_rows(Kb, 1, kr);
+            store_k(kslot1, kr);
+        }
+        __syncthreads();
+        if (group_b && wave_active(0)) scores(kslot0, s);
+        two_loops(0, [&](int t, auto mask_tag) {
+            const bool odd = t & 1;
+            uint16_t* const k_t = odd ? kslot1 : kslot0;
+            uint16_t* const k_t1 = odd ? kslot0 : kslot1;
+            uint16_t* const v_t = odd ? vslot1 : vslot0;
+            uint16_t* const v_t1 = odd ? vslot0 : vslot1;  // holds V_{t-1}
+            if (t + 2 < n_tiles) load_rows(Kb, t + 2, kr);
+            if (t + 1 < n_tiles) load_rows(Vb, t + 1, vr);
+            // phase 1
+            if (!group_b) {
+                if (pv_pending) pv(v_t1, pb);
+                pv_pending = false;
+                if (wave_active(t)) scores(k_t, s);
+            } else if (wave_active(t)) {
+                probs(s, softmax_stats(s, t, mask_tag), pb);
+            }
             __syncthreads();
-            compute(kslot0, vslot0, t, mask_tag);
+            // phase 2
+            if (!group_b) {
+                if (wave_active(t)) {
+                    probs(s, softmax_stats(s, t, mask_tag), pb);
+                    pv_pending = true;
+                }
+            } else if (wave_active(t)) {
+                pv(v_t, pb);
+                if (t + 1 < n_tiles && wave_active(t + 1)) scores(k_t1, s);
+            }
+            if (t + 2 < n_tiles) store_k(k_t, kr);
+            if (t + 1 < n_tiles) store_v(v_t1, vr);
             __syncthreads();
-        };
-        int t = 0;
-        for (; t < first_masked; ++t) step(t, std::false_type{});
-        for (; t < n_tiles; ++t) step(t, std::true_type{});
+        });
+        if (pv_pending) pv(((n_tiles - 1) & 1) ? vslot1 : vslot0, pb);
     }
 
     // ---- epilogue: O = O^T / l, one query row per lane ----------------------

@@ -11,8 +11,8 @@
 // description supplies primitive costs and capacities (architecture
 // description section).
 //
-// Here the domain is tiny (3 tile widths x 2 wave counts x 2 pipeline knobs
-// for prefill; a few dozen split counts for decode), so exhaustive
+// Here the domain is tiny (3 tile widths x 2 wave counts x 2-3 pipeline
+// knob values for prefill; a few dozen split counts for decode), so exhaustive
 // enumeration returns the exact argmin a solver would.  The prefill HEG is
 //     seq( load Q ; for(n_tiles, pipe(load K/V tile, body, -)) ; store O )
 // with body = S = K Q^T, softmax update, O += V^T P^T, and the decode HEG is
@@ -54,9 +54,9 @@ void default_desc(attn_device_desc* d) {
     d->launch_us = 4.0;
 }
 
-namespace {
-
-// HEG composition rules.
+// HEG composition rules: a pipe node with load, body and store stages and
+// the two-bit knob (load/body boundary open, body/store boundary open), and
+// a for node repeating its body.
 double heg_pipe(double load, double body, double store, int b_lm, int b_ms) {
     if (!b_lm && !b_ms) return load + body + store;
     if (!b_lm && b_ms) return std::max(load + body, store);
@@ -65,51 +65,63 @@ double heg_pipe(double load, double body, double store, int b_lm, int b_ms) {
 }
 double heg_for(double trips, double body) { return trips * body; }
 
+namespace {
+
 int round_up(int x, int a) { return (x + a - 1) / a * a; }
 
-struct FwdCost {
-    double total_cycles;
-    const char* bound;
-};
-
 // VGPRs per lane of one prefill wave: Q operand (d/4), score accumulators
-// (bn/2; a second set while the next tile's scores overlap the softmax),
-// bf16 probabilities (bn/4), output accumulator (d/2), staging registers of
-// the K and V tiles, and scalars/addresses.
-int fwd_vgprs(int d, int bn, int waves, int dbuf) {
+// (bn/2), bf16 probabilities (bn/4), output accumulator (d/2), two sets of
+// K and V operands read from LDS, staging registers of the K and V tiles, and
+// scalars/addresses.  Used only when the compiled kernel cannot be queried.
+int fwd_vgprs(int d, int bn, int waves, int pipe) {
     const int nt = waves * 64;
     const int ch = (bn * d / 8 + nt - 1) / nt;
-    const int scores = dbuf ? bn : bn / 2;
-    int v = d / 4 + scores + bn / 4 + d / 2 + 2 * ch * 4 + 24;
+    int v = d / 4 + bn / 2 + bn / 4 + d / 2 + 2 * (bn / 32) * 4 + 2 * (d / 32) * 4 +
+            (pipe ? 2 : 1) * ch * 4 + 24;
     return round_up(v, 8);
 }
 
 }  // namespace
 
+// Prefill model.  Per wave and K/V tile of BN keys:
+//   M  = MFMA cycles: 2*(BN/32)*(D/16) v_mfma_f32_32x32x16_bf16 (S and PV)
+//   V  = VALU cycles: per score one FMA, one v_exp, and a half each of
+//        v_max3, v_cvt_pk_bf16_f32 and v_dot2c (32*BN/64 scores per lane),
+//        plus a fixed part (max exchange, bookkeeping)
+//   LDS: 4*BN*D bytes read per wave (K and V operands)
+// A wave does not issue VALU work while its own MFMAs execute, but two waves
+// sharing a SIMD overlap.  Waves of one workgroup run in lockstep between
+// barriers (same phase), so with w waves per SIMD from g independent
+// workgroups the tile-round costs w*M + w*V minus the overlap
+// ((g-1)/g)*min(w*M, w*V); the ping-pong pipe (2) runs its wave pairs in
+// opposite phases, so each pair costs 2*max(M, V).  LDS bandwidth is shared
+// by the CU.  Loads of the next tile overlap compute when the pipe knob opens
+// the load/body boundary (pipe >= 1); with pipe 0 the load latency is
+// exposed to the workgroup, hidden by the other resident workgroups.
 bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d,
-                    int causal, int bn, int waves, int dbuf, FwdPlan* out, FwdResFn res) {
+                    int causal, int bn, int waves, int pipe, FwdPlan* out, FwdResFn res) {
     FwdPlan p;
     p.d = d;
     p.block_n = bn;
     p.waves = waves;
-    p.dbuf = dbuf;
+    p.pipe = pipe;
     p.causal = causal;
     p.block_m = 32 * waves;
-    p.lds_bytes = fwd_lds_bytes(d, bn, dbuf);
-    p.vgprs = fwd_vgprs(d, bn, waves, dbuf);
+    p.lds_bytes = fwd_lds_bytes(d, bn, pipe);
+    p.vgprs = fwd_vgprs(d, bn, waves, pipe);
     // legality: capacities and primitive validity
     if (bn % 32 != 0 || d % 32 != 0) return false;
+    if (pipe == 2 && waves != 8) return false;
     if (p.lds_bytes > desc.lds_bytes_per_cu) return false;
     if (p.vgprs > desc.vgprs_per_simd_lane) return false;
     const int simds = desc.simds_per_cu;
-    const int waves_per_simd_wg = std::max(1, waves / simds);
     const int wpe_regs = desc.vgprs_per_simd_lane / p.vgprs;  // waves per SIMD by registers
     int wg = desc.lds_bytes_per_cu / p.lds_bytes;
     wg = std::min(wg, (wpe_regs * simds) / waves);
     wg = std::min(wg, (desc.max_waves_per_simd * simds) / waves);
     if (res) {  // the compiled kernel's real footprint overrides the estimate
         KernelRes kr;
-        if (!res(d, bn, waves, dbuf, causal, &kr)) return false;
+        if (!res(d, bn, waves, pipe, causal, &kr)) return false;
         if (kr.scratch_bytes > 0) return false;  // spills: not a valid primitive
         wg = kr.wg_per_cu;
         if (kr.vgprs > 0) p.vgprs = kr.vgprs;
@@ -123,22 +135,29 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
     const double bm = p.block_m;
     const int cus_per_xcd = std::max(1, desc.num_cus / std::max(1, desc.num_xcds));
     const double l2_share = desc.l2_bytes_per_clk_xcd / cus_per_xcd;  // bytes/clk per CU
-    // ---- primitive costs of one K/V tile for the wg workgroups of a CU -----
-    const double mfma = wg * 4.0 * bm * bn * d / desc.mfma_bf16_flops_per_clk_cu;
+    const double mfma_cyc = 32768.0 / (desc.mfma_bf16_flops_per_clk_cu / simds);
     const double valu_op = desc.wave_size / desc.valu_lanes_per_clk_simd;  // cycles per op
     const double scores_per_lane = 32.0 * bn / desc.wave_size;
-    const double wave_valu = scores_per_lane * (4.5 * valu_op + desc.trans_cycles_per_op) +
-                             (24.0 + 0.1 * d / 2.0) * valu_op;
-    const double valu = wg * waves_per_simd_wg * wave_valu;  // per SIMD
-    const double lds_rd = wg * waves * 4.0 * bn * d / desc.lds_bytes_per_clk_cu;
-    const double lds_wr = wg * 4.0 * bn * d / desc.lds_bytes_per_clk_cu;
-    const double glob = wg * 4.0 * bn * d / l2_share;
-    const int wps = wg * waves_per_simd_wg;  // waves sharing a SIMD
-    double body = std::max(std::max(mfma, valu), lds_rd + lds_wr);
-    if (wps < 2) body = mfma + valu;  // one wave: the S->softmax->PV chain serialises
-    else body += 0.2 * std::min(mfma, valu);
-    const double tile = heg_pipe(glob, body, 0.0, dbuf, 0);
-    const double load_q = wg * bm * d * 2.0 / l2_share + glob;
+    // ---- primitive costs of one K/V tile -------------------------------
+    const double M = 2.0 * (bn / 32) * (d / 16) * mfma_cyc;
+    const double V = scores_per_lane * (2.5 * valu_op + desc.trans_cycles_per_op) + 40.0 * valu_op;
+    const double w = (double)wg * waves / simds;  // waves per SIMD
+    double compute;
+    if (pipe == 2) {
+        compute = w * std::max(M, V);
+    } else {
+        const double g = wg;
+        compute = w * (M + V) - (g - 1.0) / g * std::min(w * M, w * V);
+    }
+    const double lds = wg * waves * 4.0 * bn * d / desc.lds_bytes_per_clk_cu;
+    const double load = wg * 4.0 * bn * d / l2_share;  // K/V tile from L2
+    const double latency = desc.hbm_latency_us * 0.25 * desc.clock_ghz * 1e3;  // L2 hit
+    const double body = std::max(compute, lds);
+    // pipe node (load, body, -): knob b_lm open for pipe >= 1
+    double tile = heg_pipe(load, body, 0.0, pipe >= 1 ? 1 : 0, 0);
+    if (pipe == 0) tile += latency / wg;  // exposed, shared by the resident workgroups
+    if (pipe == 2) tile += latency / 4;   // second barrier per tile
+    const double load_q = wg * bm * d * 2.0 / l2_share + load + latency;
     const double store_o = wg * bm * d * 4.0 / l2_share;
 
     // ---- grid: regular (non-causal) or regularised (causal) --------------
@@ -149,7 +168,8 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
         const double rounds = ceil((double)p.grid / slots);
         cycles = rounds * (load_q + heg_for(full_tiles, tile) + store_o);
     } else {
-        // sum of per-q-tile work over one head, times B*H, spread over the slots
+        // per-q-tile work summed over the grid and spread over the slots,
+        // plus the longest workgroup as a tail term
         double sum_tiles = 0.0;
         int max_tiles = 0;
         for (int qt = 0; qt < p.n_qtiles; ++qt) {
@@ -162,7 +182,7 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
         const double per_wg_fixed = load_q + store_o;
         const double work = (double)B * H * (sum_tiles * tile + p.n_qtiles * per_wg_fixed);
         const double longest = per_wg_fixed + heg_for(max_tiles, tile);
-        cycles = (p.grid > slots) ? work / slots + 0.5 * longest : longest;
+        cycles = std::max(work / slots + 0.25 * longest, longest);
     }
     double us = cycles / (desc.clock_ghz * 1e3);
     const double bytes = (double)B * H * ((double)Sq * d * 6.0 + (double)Skv * d * 4.0);
@@ -171,16 +191,14 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
     if (hbm_us > us) {
         us = hbm_us;
         bound = "hbm";
-    } else if (dbuf && glob > body) {
+    } else if (pipe >= 1 && load > body) {
         bound = "l2";
-    } else if (wps < 2) {
-        bound = "mfma+valu";
-    } else if (mfma >= valu && mfma >= lds_rd + lds_wr) {
-        bound = "mfma";
-    } else if (valu >= lds_rd + lds_wr) {
-        bound = "valu";
-    } else {
+    } else if (lds > compute) {
         bound = "lds";
+    } else if (w * M >= w * V) {
+        bound = "mfma";
+    } else {
+        bound = "valu";
     }
     p.modeled_us = us + desc.launch_us;
     p.bound = bound;
@@ -194,9 +212,9 @@ bool plan_fwd(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d
     FwdPlan best;
     for (int bn : kFwdBlockN)
         for (int waves : kFwdWaves)
-            for (int dbuf : kFwdDbuf) {
+            for (int pipe : kFwdPipe) {
                 FwdPlan p;
-                if (!plan_fwd_fixed(desc, B, H, Sq, Skv, d, causal, bn, waves, dbuf, &p, res))
+                if (!plan_fwd_fixed(desc, B, H, Sq, Skv, d, causal, bn, waves, pipe, &p, res))
                     continue;
                 // strict improvement keeps the first (smallest) candidate on ties
                 if (!found || p.modeled_us < best.modeled_us * (1.0 - 1e-9)) {
@@ -270,11 +288,22 @@ bool plan_decode(const attn_device_desc& desc, int B, int H, int Skv, int d, int
     return found;
 }
 
+}  // namespace attn
+
+// Internal symbols for unit tests of the composition rules (not part of the
+// public header).
+extern "C" double attn__heg_pipe(double load, double body, double store, int b_lm, int b_ms) {
+    return attn::heg_pipe(load, body, store, b_lm, b_ms);
+}
+extern "C" double attn__heg_for(double trips, double body) { return attn::heg_for(trips, body); }
+
+namespace attn {
+
 int format_fwd_plan(const FwdPlan& p, char* buf, int buflen) {
     return snprintf(buf, buf ? (size_t)buflen : 0,
-                    "kind=fwd d=%d BLOCK_M=%d BLOCK_N=%d WAVES=%d DBUF=%d causal=%d grid=%lld "
+                    "kind=fwd d=%d BLOCK_M=%d BLOCK_N=%d WAVES=%d PIPE=%d causal=%d grid=%lld "
                     "n_qtiles=%d lds_bytes=%d vgprs=%d wg_per_cu=%d modeled_us=%.3f bound=%s",
-                    p.d, p.block_m, p.block_n, p.waves, p.dbuf, p.causal, p.grid, p.n_qtiles,
+                    p.d, p.block_m, p.block_n, p.waves, p.pipe, p.causal, p.grid, p.n_qtiles,
                     p.lds_bytes, p.vgprs, p.wg_per_cu, p.modeled_us, p.bound);
 }
 

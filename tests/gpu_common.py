@@ -38,8 +38,8 @@ def compare(got, want, what: str, max_abs: float = MAX_ABS, mean_abs: float = ME
 class forced_plan:
     """Context manager fixing the prefill tile (the ablation hook)."""
 
-    def __init__(self, bn: int, waves: int, dbuf: int):
-        self.value = f"bn={bn},waves={waves},dbuf={dbuf}"
+    def __init__(self, bn: int, waves: int, pipe: int):
+        self.value = f"bn={bn},waves={waves},pipe={pipe}"
 
     def __enter__(self):
         self.old = os.environ.get("ATTN_FORCE_PLAN")

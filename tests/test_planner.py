@@ -1,0 +1,141 @@
+"""CPU tests of the analytic planner (HEG composition + constrained argmin).
+
+The composition rules are the paper's latency-modelling equations: a
+sequential composition adds, a for node multiplies by its trip count, and a
+pipe node with load/body/store stages takes a sum or a max according to its
+two-bit knob (Eq. heg-seq, heg-for, heg-pipe).  The rest checks properties
+of the constrained argmin over the candidate domain (Eq. heg-optimization,
+global-candidate-selection) on synthetic device descriptions.
+"""
+import ctypes
+import itertools
+
+import pytest
+
+import paper_2609_29219_amd as pa
+
+heg_pipe = pa.lib.attn__heg_pipe
+heg_pipe.argtypes = [ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_int, ctypes.c_int]
+heg_pipe.restype = ctypes.c_double
+heg_for = pa.lib.attn__heg_for
+heg_for.argtypes = [ctypes.c_double, ctypes.c_double]
+heg_for.restype = ctypes.c_double
+
+
+@pytest.mark.parametrize("l,m,s", [(3.0, 5.0, 2.0), (7.0, 1.0, 1.0), (1.0, 1.0, 9.0), (0.0, 4.0, 0.0)])
+def test_heg_pipe_knob_cases(l, m, s):
+    assert heg_pipe(l, m, s, 0, 0) == l + m + s          # both boundaries closed: one serial stage
+    assert heg_pipe(l, m, s, 0, 1) == max(l + m, s)      # body/store open
+    assert heg_pipe(l, m, s, 1, 0) == max(l, m + s)      # load/body open
+    assert heg_pipe(l, m, s, 1, 1) == max(l, m, s)       # fully pipelined
+
+
+def test_heg_pipe_open_boundaries_never_slower():
+    for l, m, s in itertools.product((0.5, 2.0, 7.0), repeat=3):
+        closed = heg_pipe(l, m, s, 0, 0)
+        for b in ((0, 1), (1, 0), (1, 1)):
+            assert heg_pipe(l, m, s, *b) <= closed
+        assert heg_pipe(l, m, s, 1, 1) <= min(heg_pipe(l, m, s, 0, 1), heg_pipe(l, m, s, 1, 0))
+
+
+def test_heg_for_multiplies():
+    assert heg_for(7, 3.5) == 24.5
+    assert heg_for(0, 9.0) == 0.0
+
+
+def spec():
+    d = pa.DeviceDesc()
+    pa.lib.attn_query_device(ctypes.byref(d))
+    d.arch = b"gfx950"
+    return d
+
+
+def plan(desc, kind, B, H, Sq, Skv, d, causal=False, n=0):
+    return pa.parse_plan(pa.get_plan(kind, B, H, Sq, Skv, d, causal, n, desc=desc))
+
+
+WORKLOADS = [(pa.KIND_FWD, 1, 1, 256, 256, 64, False), (pa.KIND_FWD, 4, 16, 2048, 2048, 128, True),
+             (pa.KIND_FWD, 1, 32, 8192, 8192, 128, False), (pa.KIND_DECODE, 16, 32, 1, 8192, 128, False),
+             (pa.KIND_DECODE, 1, 32, 1, 131072, 128, False)]
+
+
+@pytest.mark.parametrize("w", WORKLOADS)
+def test_plan_is_deterministic_and_named(w):
+    a = pa.get_plan(*w, desc=spec())
+    b = pa.get_plan(*w, desc=spec())
+    assert a == b
+    p = pa.parse_plan(a)
+    assert p["modeled_us"] > 0 and p["bound"]
+    if w[0] == pa.KIND_FWD:
+        assert p["BLOCK_N"] in (32, 64, 128) and p["WAVES"] in (4, 8) and p["PIPE"] in (0, 1, 2)
+        assert p["PIPE"] < 2 or p["WAVES"] == 8
+        assert p["BLOCK_M"] == 32 * p["WAVES"]
+        assert p["lds_bytes"] <= 160 * 1024
+    else:
+        assert 1 <= p["N_SPLITS"] <= w[4]
+        assert (w[4] + p["CHUNK"] - 1) // p["CHUNK"] == p["N_SPLITS"]  # every split non-empty
+
+
+def test_lds_capacity_constrains_the_tile():
+    d = spec()
+    for cap in (160 * 1024, 72 * 1024, 40 * 1024, 20 * 1024):
+        d.lds_bytes_per_cu = cap
+        p = plan(d, pa.KIND_FWD, 1, 32, 8192, 8192, 128)
+        assert p["lds_bytes"] <= cap
+    d.lds_bytes_per_cu = 8 * 1024  # nothing fits
+    with pytest.raises(pa.AttnError) as e:
+        plan(d, pa.KIND_FWD, 1, 32, 8192, 8192, 128)
+    assert e.value.code == pa.ATTN_EUNSUPPORTED
+
+
+def test_register_file_constrains_the_tile():
+    d = spec()
+    d.vgprs_per_simd_lane = 200
+    p = plan(d, pa.KIND_FWD, 1, 32, 8192, 8192, 128)
+    assert p["vgprs"] <= 200
+
+
+def test_causal_models_about_half_the_work():
+    d = spec()
+    nc = plan(d, pa.KIND_FWD, 4, 16, 2048, 2048, 128, False)["modeled_us"]
+    c = plan(d, pa.KIND_FWD, 4, 16, 2048, 2048, 128, True)["modeled_us"]
+    assert 0.35 * nc < c < 0.8 * nc
+
+
+def test_modeled_time_grows_with_work():
+    d = spec()
+    t = [plan(d, pa.KIND_FWD, 1, h, 4096, 4096, 128)["modeled_us"] for h in (8, 32, 128)]
+    assert t[0] < t[1] < t[2]
+
+
+def test_decode_splits_follow_compute_units():
+    d = spec()
+    last = 0
+    for cus in (16, 64, 256, 1024):
+        d.num_cus = cus
+        n = plan(d, pa.KIND_DECODE, 1, 32, 1, 131072, 128)["N_SPLITS"]
+        assert n >= last
+        last = n
+    assert last > 1  # one head per workgroup cannot fill 1024 CUs
+
+
+def test_decode_explicit_splits_are_clamped():
+    d = spec()
+    assert plan(d, pa.KIND_DECODE, 1, 1, 1, 100, 128, n=7)["N_SPLITS"] == 7
+    assert plan(d, pa.KIND_DECODE, 1, 1, 1, 100, 128, n=1000)["N_SPLITS"] == 100
+    assert plan(d, pa.KIND_DECODE, 1, 1, 1, 10, 128, n=3)["CHUNK"] == 4
+
+
+def test_decode_split_count_is_bounded_by_keys():
+    d = spec()
+    for skv in (1, 5, 127, 128, 4096):
+        p = plan(d, pa.KIND_DECODE, 1, 1, 1, skv, 64)
+        assert 1 <= p["N_SPLITS"] <= skv
+
+
+def test_bad_descriptions_rejected():
+    d = spec()
+    d.num_cus = 0
+    with pytest.raises(pa.AttnError) as e:
+        plan(d, pa.KIND_FWD, 1, 1, 64, 64, 64)
+    assert e.value.code == pa.ATTN_EINVAL
