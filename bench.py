@@ -19,6 +19,7 @@ prefill workload, timed on this host's cores.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import platform
@@ -30,6 +31,39 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2516.6  # 256 CU x 4096 flop/clk x 2.4 GHz (dense bf16 MFMA)
 PEAK_HBM_GBS = 8000.0      # HBM3E
+
+PROFILES = os.path.join(ROOT, "profiles")
+CSRC = os.path.join(ROOT, "paper_2609_29219_amd", "csrc")
+# sources that decide which kernel runs and what it does
+KERNEL_SOURCES = {
+    "prefill": ("fwd_kernel.h", "fwd_d128.hip", "fwd_d64.hip", "plan.cpp", "api.hip", "common.h"),
+    "decode": ("decode.hip", "plan.cpp", "api.hip", "common.h"),
+}
+
+
+def source_hash(kind: str) -> str:
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES[kind]:
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def profiled_traffic(kind: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 summary, or None if the
+    kernel sources changed since the counters were taken."""
+    path = os.path.join(PROFILES, f"traffic_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as f:
+        for line in f:
+            if "=" in line and not line.startswith("#"):
+                k, _, v = line.strip().partition("=")
+                fields[k.strip()] = v.strip()
+    if fields.get("source_sha256") != source_hash(kind):
+        return None
+    return int(fields["traffic_bytes_per_launch"])
 
 
 def _args():
@@ -190,12 +224,15 @@ def main():
                                "causal": wp.causal, "plan": fplan},
                    "decode": {"B": wd.B, "H": wd.H, "Skv": wd.Skv, "d": wd.d, "plan": dplan}},
         "roofline": {"bound": "mfma", "achieved": tflops, "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": tflops / PEAK_BF16_TFLOPS, "traffic": None,
+                     "unit": "TFLOP/s", "frac": tflops / PEAK_BF16_TFLOPS,
+                     "traffic": profiled_traffic("prefill", wp.name),
+                     "algorithmic_bytes": wp.hbm_bytes(),
                      "kernel": "fwd_kernel", "ms_per_launch": fwd_ms,
                      "flops_per_launch": wp.flops()},
         "decode": {"value": gbs, "unit": "GB/s", "ms_per_call": dec_ms,
                    "roofline": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS,
-                                "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS, "traffic": None,
+                                "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS,
+                                "traffic": profiled_traffic("decode", wd.name),
                                 "kernel": "decode_partial_kernel + decode_combine_kernel",
                                 "bytes_per_call": wd.hbm_bytes()}},
     }

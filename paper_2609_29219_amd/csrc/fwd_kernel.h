@@ -148,14 +148,22 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     const int xcd = wg % num_xcds, slot_id = wg / num_xcds;
     const int logical =
         (xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per) + slot_id;
-    const int bh = logical / n_qtiles;
-    const int qt_order = logical % n_qtiles;
-    // causal: heaviest q-tiles (most keys) first within each head
-    const int qt = CAUSAL ? (n_qtiles - 1 - qt_order) : qt_order;
+    // Causal work grows linearly with the q-tile index, so a causal
+    // workgroup takes the pair of q-tiles (n-1-u, u): every workgroup then
+    // holds n+1 tiles of work (heavy one first).  Non-causal: one q-tile.
+    const int units = CAUSAL ? (n_qtiles + 1) / 2 : n_qtiles;
+    const int bh = logical / units;
+    const int unit = logical % units;
+    const int n_pass = (CAUSAL && n_qtiles - 1 - unit != unit) ? 2 : 1;
+    const int diag = Skv - Sq;  // causal: key j allowed iff j <= row + diag
+    const long long kv_base = (long long)bh * Skv * D;
+    const uint16_t* Kb = K + kv_base;
+    const uint16_t* Vb = V + kv_base;
 
+    for (int pass = 0; pass < n_pass; ++pass) {
+    const int qt = CAUSAL ? (pass == 0 ? n_qtiles - 1 - unit : unit) : unit;
     const int q_wave0 = qt * BM + wave * 32;  // first query row of this wave
     const int qrow = q_wave0 + l32;
-    const int diag = Skv - Sq;                // causal: key j allowed iff j <= row + diag
 
     // ---- Q tile into VGPRs, as the B operand (16 dims x 32 queries) --------
     bf16x8 qf[KD];
@@ -182,10 +190,6 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     // tiles before first_masked need no mask for any row of this workgroup
     int first_masked = Skv / BN;  // the ragged tail tile, if any
     if (CAUSAL) first_masked = min(first_masked, (qt * BM + diag + 1) / BN);
-
-    const long long kv_base = (long long)bh * Skv * D;
-    const uint16_t* Kb = K + kv_base;
-    const uint16_t* Vb = V + kv_base;
 
     // Rows past the end of the key range are loaded from the last valid row
     // (clamped, never out of bounds): their scores are masked to weight 0,
@@ -458,6 +462,8 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
                 *reinterpret_cast<float4*>(orow + cb * 32 + 8 * g) = val;
             }
     }
+    __syncthreads();  // the next q-tile refills LDS slots read above
+    }  // pass
 }
 
 }  // namespace attn

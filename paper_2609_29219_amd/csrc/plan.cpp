@@ -129,7 +129,8 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
     if (wg < 1) return false;
     p.wg_per_cu = wg;
     p.n_qtiles = (Sq + p.block_m - 1) / p.block_m;
-    p.grid = (long long)B * H * p.n_qtiles;
+    // causal workgroups take q-tile pairs (n-1-u, u)
+    p.grid = (long long)B * H * (causal ? (p.n_qtiles + 1) / 2 : p.n_qtiles);
     if (p.grid > 0x7fffffffLL) return false;
 
     const double bm = p.block_m;
@@ -168,21 +169,24 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
         const double rounds = ceil((double)p.grid / slots);
         cycles = rounds * (load_q + heg_for(full_tiles, tile) + store_o);
     } else {
-        // per-q-tile work summed over the grid and spread over the slots,
-        // plus the longest workgroup as a tail term
-        double sum_tiles = 0.0;
-        int max_tiles = 0;
-        for (int qt = 0; qt < p.n_qtiles; ++qt) {
+        // workgroups take q-tile pairs (n-1-u, u), which regularises the
+        // triangular work: per workgroup the sum of the pair's tile counts
+        auto tiles_of = [&](int qt) {
             const int last_q = std::min(qt * p.block_m + p.block_m - 1, Sq - 1);
             const int kv_end = std::min(Skv, last_q + (Skv - Sq) + 1);
-            const int nt = (kv_end + bn - 1) / bn;
-            sum_tiles += nt;
-            max_tiles = std::max(max_tiles, nt);
+            return (kv_end + bn - 1) / bn;
+        };
+        double sum = 0.0, longest = 0.0;
+        const int units = (p.n_qtiles + 1) / 2;
+        for (int u = 0; u < units; ++u) {
+            const int heavy = p.n_qtiles - 1 - u;
+            double t = load_q + store_o + heg_for(tiles_of(heavy), tile);
+            if (heavy != u) t += load_q + store_o + heg_for(tiles_of(u), tile);
+            sum += t;
+            longest = std::max(longest, t);
         }
-        const double per_wg_fixed = load_q + store_o;
-        const double work = (double)B * H * (sum_tiles * tile + p.n_qtiles * per_wg_fixed);
-        const double longest = per_wg_fixed + heg_for(max_tiles, tile);
-        cycles = std::max(work / slots + 0.25 * longest, longest);
+        const double rounds = ceil((double)p.grid / slots);
+        cycles = std::max(rounds * sum / units, longest);
     }
     double us = cycles / (desc.clock_ghz * 1e3);
     const double bytes = (double)B * H * ((double)Sq * d * 6.0 + (double)Skv * d * 4.0);
