@@ -15,7 +15,8 @@ struct FwdPlan {
     int block_m = 0;    // queries per workgroup (32 per wave)
     int block_n = 0;    // keys per K/V tile staged in LDS
     int waves = 0;      // waves per workgroup
-    int pipe = 0;       // 0 serial, 1 next tile prefetched, 2 ping-pong wave groups
+    int pipe = 0;       // 0 serial, 1 next tile prefetched, 2 ping-pong wave groups,
+                        // 3 software pipeline (softmax between MFMAs)
     int causal = 0;
     int lds_bytes = 0;  // per workgroup
     int vgprs = 0;      // modelled VGPRs per lane
@@ -42,12 +43,12 @@ struct DecodePlan {
 // Candidate domains: every point is an instantiated kernel.
 constexpr int kFwdBlockN[] = {32, 64, 128};
 constexpr int kFwdWaves[] = {4, 8};
-constexpr int kFwdPipe[] = {0, 1, 2};  // 2 only with 8 waves
+constexpr int kFwdPipe[] = {0, 1, 2, 3};  // 2 only with 8 waves, 3 only with BN <= 64
 constexpr int kDecodeThreads = 256;
 constexpr int kDecodeUnroll = 8;
 
 // LDS footprint of a prefill workgroup: K tile [BN][D+8] and V tile
-// [BN][D+32] in bf16, one slot each (pipe 0) or two (pipe 1, 2).
+// [BN][D+32] in bf16, one slot each (pipe 0) or two (pipe 1, 2, 3).
 constexpr int fwd_lds_bytes(int d, int bn, int pipe) {
     return (pipe == 0 ? 1 : 2) * (bn * (d + 8) + bn * (d + 32)) * 2;
 }

@@ -18,6 +18,7 @@ static bool with_variant(int bn, int waves, int pipe, int causal, F& f) {
     ATTN_V(32, 4, 0) ATTN_V(32, 4, 1) ATTN_V(32, 8, 0) ATTN_V(32, 8, 1) ATTN_V(32, 8, 2)
     ATTN_V(64, 4, 0) ATTN_V(64, 4, 1) ATTN_V(64, 8, 0) ATTN_V(64, 8, 1) ATTN_V(64, 8, 2)
     ATTN_V(128, 4, 0) ATTN_V(128, 4, 1) ATTN_V(128, 8, 0) ATTN_V(128, 8, 1) ATTN_V(128, 8, 2)
+    ATTN_V(32, 4, 3) ATTN_V(32, 8, 3) ATTN_V(64, 4, 3) ATTN_V(64, 8, 3)
 #undef ATTN_V
     return false;
 }

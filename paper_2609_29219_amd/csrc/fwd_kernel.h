@@ -34,17 +34,24 @@
 // four rows a transposed read touches start 16 banks apart and its 32 lanes
 // per cycle (two 16-lane groups 8 banks apart) cover all 64 banks.
 //
+// Tile loads.  Pipes 0, 1 and 3 load K/V tiles straight from global memory
+// into LDS (global_load_lds_dwordx4), with the K permutation and the padding
+// expressed in the per-lane source addresses; pipe 2 stages them through
+// registers.
+//
 // Pipelining (the HEG pipe knob, PIPE):
 //   0  one LDS slot per operand: load -> barrier -> compute -> barrier; any
 //      overlap comes from the other workgroups resident on the CU.
-//   1  two slots: the global loads of tile t+1 are in flight while tile t is
-//      computed, then written to the other slot; one barrier per tile.
-//   2  ping-pong (8 waves): a wave cannot issue vector instructions while its
-//      own MFMAs execute, but the two waves sharing a SIMD can.  Waves 0-3
-//      (group A) and 4-7 (group B, one of each per SIMD) therefore run in
-//      opposite phases: while A issues the MFMAs of PV(t-1) and S(t), B runs
-//      the softmax of tile t on the VALU, and the other way round in the
-//      second half of the tile; two barriers per tile.
+//   1  two slots: tile t+1 streams into the other slot while tile t is
+//      computed; one barrier per tile.
+//   2  ping-pong (8 waves): waves 0-3 (group A) and 4-7 (group B, one of each
+//      per SIMD) run in opposite phases: while A issues the MFMAs of PV(t-1)
+//      and S(t), B runs the softmax of tile t on the VALU, and the other way
+//      round in the second half of the tile; two barriers per tile.
+//   3  software pipeline: each wave issues the MFMAs of S(t+1) and PV(t) one
+//      by one with the softmax VALU work of tile t between them (a wave issues
+//      in order, so the matrix core and the VALU work together only if the
+//      instruction stream interleaves them); one barrier per tile.
 // Only the tiles that hold the ragged end of the key range or cross the
 // workgroup's causal diagonal run the masking code.
 //
@@ -101,6 +108,15 @@ __device__ __forceinline__ s16x4 lds_read_tr(const uint16_t* p) {
         (__attribute__((address_space(3))) s16x4*)(p));
 }
 
+// Compile-time loop: f(std::integral_constant<int, I>{}) for I in [B, E).
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        static_for<B + 1, E>(f);
+    }
+}
+
 constexpr int fwd_slots(int pipe) { return pipe == 0 ? 1 : 2; }
 
 // Waves per SIMD the register allocator should leave room for: two when two
@@ -118,6 +134,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     const uint16_t* __restrict__ V, float* __restrict__ O, int Sq, int Skv, int n_qtiles,
     int n_wg, int num_xcds, float scale_log2, uint32_t q_sign) {
     static_assert(PIPE != 2 || NW == 8, "the ping-pong schedule pairs 4 waves with 4 waves");
+    static_assert(PIPE != 3 || BN <= 64, "two score tiles in registers");
     constexpr int BM = NW * 32;
     constexpr int NT = NW * 64;
     constexpr int KD = D / 16;   // MFMA k-steps over the head dimension
@@ -186,7 +203,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     }
     const int n_tiles = (kv_end + BN - 1) / BN;
     // causal: a tile entirely above this wave's diagonal is skipped
-    auto wave_active = [&](int t) { return !CAUSAL || t * BN <= q_wave0 + 31 + diag; };
+    auto wave_active = [&](int t) __attribute__((always_inline)) { return !CAUSAL || t * BN <= q_wave0 + 31 + diag; };
     // tiles before first_masked need no mask for any row of this workgroup
     int first_masked = Skv / BN;  // the ragged tail tile, if any
     if (CAUSAL) first_masked = min(first_masked, (qt * BM + diag + 1) / BN);
@@ -194,7 +211,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     // Rows past the end of the key range are loaded from the last valid row
     // (clamped, never out of bounds): their scores are masked to weight 0,
     // and their V values are finite, so they contribute exactly 0.
-    auto load_rows = [&](const uint16_t* base, int t, u32x4 (&reg)[CH]) {
+    auto load_rows = [&](const uint16_t* base, int t, u32x4 (&reg)[CH]) __attribute__((always_inline)) {
         const int key0 = t * BN;
 #pragma unroll
         for (int i = 0; i < CH; ++i) {
@@ -206,7 +223,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
             }
         }
     };
-    auto store_k = [&](uint16_t* dst, const u32x4 (&reg)[CH]) {
+    auto store_k = [&](uint16_t* dst, const u32x4 (&reg)[CH]) __attribute__((always_inline)) {
 #pragma unroll
         for (int i = 0; i < CH; ++i) {
             const int u = tid + i * NT;
@@ -217,7 +234,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
             }
         }
     };
-    auto store_v = [&](uint16_t* dst, const u32x4 (&reg)[CH]) {
+    auto store_v = [&](uint16_t* dst, const u32x4 (&reg)[CH]) __attribute__((always_inline)) {
 #pragma unroll
         for (int i = 0; i < CH; ++i) {
             const int u = tid + i * NT;
@@ -226,6 +243,53 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
                 *reinterpret_cast<u32x4*>(dst + j * L::V_STRIDE + cc * 8) = reg[i];
             }
         }
+    };
+
+    // Direct global -> LDS tile loads (pipes 0, 1, 3).  global_load_lds_dwordx4
+    // writes lane i's 16 bytes at the wave-uniform LDS base + 16*i, so a tile
+    // region (its padded rows laid end to end) is filled in 1 KiB pieces, and
+    // each lane picks the source chunk that belongs at its position: the K row
+    // permutation and the padding live in the source addresses (a padding
+    // position re-reads a chunk of its own row).  No registers carry tile
+    // data, and the loads complete behind the barrier that publishes them.
+    constexpr int DCH = D / 8;                                   // 16-byte chunks of a row
+    constexpr int KST = L::K_STRIDE / 8, VST = L::V_STRIDE / 8;  // per padded LDS row
+    constexpr int KCH = BN * KST, VCH = BN * VST;                // positions per region
+    constexpr int KI = (KCH + 63) / 64, VI = (VCH + 63) / 64;    // pieces per region
+    constexpr int KJ = (KI + NW - 1) / NW, VJ = (VI + NW - 1) / NW;  // pieces per wave
+    // element offset of this lane's source chunk inside a tile, -1 for none
+    int koff[KJ], voff[VJ];
+#pragma unroll
+    for (int j = 0; j < KJ; ++j) {
+        const int i = wave + j * NW, pos = i * 64 + lane;
+        const int prow = pos / KST, key = (prow & ~31) | (16 * ((prow & 7) >> 2) +
+                                                          4 * ((prow & 31) >> 3) + (prow & 3));
+        koff[j] = (i < KI && pos < KCH) ? key * D + min(pos % KST, DCH - 1) * 8 : -1;
+    }
+#pragma unroll
+    for (int j = 0; j < VJ; ++j) {
+        const int i = wave + j * NW, pos = i * 64 + lane;
+        voff[j] = (i < VI && pos < VCH) ? (pos / VST) * D + min(pos % VST, DCH - 1) * 8 : -1;
+    }
+    auto dma_tile = [&](const uint16_t* base, int t, uint16_t* dst, const int* off, int nj,
+                        int ni) __attribute__((always_inline)) {
+        const int key0 = t * BN;
+        const bool ragged = key0 + BN > Skv;  // rows past the end re-read the last key
+        const uint16_t* tb = base + (long long)key0 * D;
+        for (int j = 0; j < nj; ++j) {
+            const int i = wave + j * NW;
+            if (i < ni && off[j] >= 0) {
+                int o = off[j];
+                if (ragged) o = (min(key0 + o / D, Skv - 1) - key0) * D + o % D;
+                __builtin_amdgcn_global_load_lds(tb + o, dst + i * 512, 16, 0, 0);
+            }
+        }
+    };
+    auto dma_k = [&](int t, uint16_t* dst) __attribute__((always_inline)) {
+        dma_tile(Kb, t, dst, koff, KJ, KI);
+    };
+    auto dma_v = [&](int t, uint16_t* dst) __attribute__((always_inline)) {
+        dma_tile(Vb, t, dst, voff, VJ, VI);
     };
 
     // ---- online-softmax state (one query row per lane) --------------------
@@ -238,7 +302,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
         for (int r = 0; r < 16; ++r) oacc[cb][r] = 0.f;
 
     // S^T = K Q^T for one tile (independent accumulators interleaved).
-    auto scores = [&](const uint16_t* kl, f32x16 (&s)[KB]) {
+    auto scores = [&](const uint16_t* kl, f32x16 (&s)[KB]) __attribute__((always_inline)) {
         const uint16_t* ka_base = kl + l32 * L::K_STRIDE + hh * 8;
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb)
@@ -253,22 +317,15 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
             }
     };
 
-    // Online-softmax statistics of tile t: mask (MASK tiles only), row max,
-    // and the lazy rescale.  The running max m_i of a row only moves when the
-    // tile's max exceeds it by more than kRescaleSlack (log2 units), so the
-    // output rescale is skipped on almost every tile; probabilities are then
-    // bounded by 2^kRescaleSlack, and the numerator and the normaliser share
-    // the same reference, so the result is unchanged.  Returns the reference
-    // to subtract.
-    auto softmax_stats = [&](f32x16 (&s)[KB], int t, auto mask_tag) -> float {
+    // Row max of a tile's scores (masked in place on MASK tiles: the ragged
+    // end of the key range and, on diagonal tiles, causality).  Register r of
+    // block kb holds key key0 + 16*hh + (kb*32 + r), so the constant kb*32 + r
+    // is compared against one per-lane bound.
+    auto tile_max = [&](f32x16 (&s)[KB], int t, auto mask_tag) __attribute__((always_inline)) -> float {
         constexpr bool MASK = decltype(mask_tag)::value;
-        const int key0 = t * BN;
         if (MASK) {
-            // ragged tail of the key range and, on diagonal tiles, causality:
-            // register r of block kb holds key key0 + 16*hh + (kb*32 + r), so
-            // compare the constant kb*32 + r against one per-lane bound
             const int lim = CAUSAL ? min(Skv - 1, qrow + diag) : Skv - 1;
-            const int room = lim - key0 - 16 * hh;
+            const int room = lim - t * BN - 16 * hh;
 #pragma unroll
             for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
@@ -280,7 +337,15 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
         for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
             for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
-        mx = half_swap_max(mx);
+        return half_swap_max(mx);
+    };
+    // Lazy rescale: the running max m_i of a row only moves when a tile's max
+    // exceeds it by more than kRescaleSlack (log2 units), so the output
+    // rescale is skipped on almost every tile; probabilities are then bounded
+    // by 2^kRescaleSlack, and the numerator and the normaliser share the same
+    // reference, so the result is unchanged.  Returns the reference to
+    // subtract (0 while the row has seen no allowed key).
+    auto update_ref = [&](float mx) __attribute__((always_inline)) -> float {
         const float tmax = (mx == -INFINITY) ? -INFINITY : mx * scale_log2;
         const bool move = tmax > m_i + kRescaleSlack;  // also true for the first finite max
         if (__any(move)) {
@@ -295,33 +360,42 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
         }
         return (m_i == -INFINITY) ? 0.f : m_i;
     };
-    // bf16 probabilities of a tile and their sum (VALU only).  Masked scores
-    // are -inf and the scale is > 0, so they give exactly 0.
-    auto probs = [&](const f32x16 (&s)[KB], float m_ref, bf16x8 (&pb)[KB][2]) {
-        float rs = 0.f;
+    auto softmax_stats = [&](f32x16 (&s)[KB], int t, auto mask_tag) __attribute__((always_inline)) -> float {
+        return update_ref(tile_max(s, t, mask_tag));
+    };
+    // bf16 probabilities of a tile (VALU only) and their sum.  The sum is
+    // taken over the rounded values (bf16 -> fp32 is a shift or a mask), so
+    // the weights applied to V sum exactly to the normaliser: the output is a
+    // convex combination of V rows up to fp32 rounding.  Masked scores are
+    // -inf and the scale is > 0, so they give exactly 0.
+    auto rounded_pair = [&](float x0, float x1, bf16x8& dst, int e, float& r0, float& r1)
+        __attribute__((always_inline)) {
+        dst[e] = (__bf16)x0;
+        dst[e + 1] = (__bf16)x1;
+        const uint32_t w = __builtin_bit_cast(uint32_t, bf16x2{dst[e], dst[e + 1]});
+        r0 += __uint_as_float(w << 16);
+        r1 += __uint_as_float(w & 0xffff0000u);
+    };
+    auto probs = [&](const f32x16 (&s)[KB], float m_ref, bf16x8 (&pb)[KB][2])
+        __attribute__((always_inline)) {
+        float rs0 = 0.f, rs1 = 0.f;
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-            for (int h2 = 0; h2 < 2; ++h2) {
+            for (int h2 = 0; h2 < 2; ++h2)
 #pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    pb[kb][h2][e] =
-                        (__bf16)__builtin_amdgcn_exp2f(fmaf(s[kb][8 * h2 + e], scale_log2, -m_ref));
-                // sum of the rounded probabilities (bf16 -> fp32 is a shift or a
-                // mask); plain adds co-issue with another wave's MFMAs, which the
-                // bf16 dot-product instructions do not
-                const u32x4 w = __builtin_bit_cast(u32x4, pb[kb][h2]);
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    rs += __uint_as_float(w[e] << 16) + __uint_as_float(w[e] & 0xffff0000u);
-            }
-        l_i += rs;
+                for (int e = 0; e < 8; e += 2)
+                    rounded_pair(
+                        __builtin_amdgcn_exp2f(fmaf(s[kb][8 * h2 + e], scale_log2, -m_ref)),
+                        __builtin_amdgcn_exp2f(fmaf(s[kb][8 * h2 + e + 1], scale_log2, -m_ref)),
+                        pb[kb][h2], e, rs0, rs1);
+        l_i += rs0 + rs1;
     };
 
     // O^T += V^T P^T in groups of 8 keys; V^T operands by transposed reads.
     const int tr_row = (lane & 15) >> 2;                         // + k0
     const int tr_col = ((lane >> 4) & 1) * 16 + 4 * (lane & 3);  // + cb*32
-    auto pv = [&](const uint16_t* vl, const bf16x8 (&pb)[KB][2]) {
+    auto pv = [&](const uint16_t* vl, const bf16x8 (&pb)[KB][2]) __attribute__((always_inline)) {
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
@@ -339,23 +413,123 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
             }
     };
 
+    // One tile t of the software pipeline.  The MFMAs of S(t+1) (K_{t+1}
+    // from kl, into s_nxt; HAS_S only) and then of PV(t) (V_t from vl) are
+    // issued one by one; between them, in program order, sit the
+    // exponentials of tile t (scores s_cur, reference m_ref, probabilities
+    // into pb) and, once S(t+1) is complete, the row max of tile t+1 (masked
+    // in place first on MASK_NEXT tiles), which is returned.  Probabilities of
+    // a 16-key step are produced before the PV MFMAs that consume them.  LDS
+    // operands are fetched PF MFMAs ahead, which also bounds their registers.
+    auto fused_tile = [&](const uint16_t* kl, const uint16_t* vl, const f32x16 (&s_cur)[KB],
+                          f32x16 (&s_nxt)[KB], bf16x8 (&pb)[KB][2], int t, float m_ref,
+                          auto has_s_tag, auto mask_tag) __attribute__((always_inline)) -> float {
+        constexpr bool HAS_S = decltype(has_s_tag)::value;
+        constexpr bool MASK_NEXT = decltype(mask_tag)::value;
+        constexpr int NS = HAS_S ? KB * KD : 0;  // MFMAs of S(t+1)
+        constexpr int NPV = KB * 2 * CB;          // MFMAs of PV(t)
+        constexpr int NM = NS + NPV;
+        constexpr int PF = 3;
+        constexpr int NPAIR = KB * 8;                    // pairs of probabilities per lane
+        constexpr int EXP_SLOTS = HAS_S ? NS + NPV / 2 : 0;  // slots carrying exponentials
+        constexpr int MAX0 = EXP_SLOTS + 1;              // first slot carrying the next max
+        constexpr int NMAXV = HAS_S ? KB * 16 : 0;      // scores of tile t+1 per lane
+        static_assert(!HAS_S || MAX0 < NM, "too few MFMAs to carry the softmax");
+        // pair pp (16-key step pp / 4) is computed in slot pp * EXP_SLOTS / NPAIR,
+        // before the first PV MFMA of its step, NS + (pp / 4) * CB
+        static_assert(!HAS_S || (NPAIR - 1) * EXP_SLOTS / NPAIR < NS + ((NPAIR - 1) / 4) * CB,
+                      "probabilities must precede their PV MFMAs");
+        auto fetch = [&](int i) __attribute__((always_inline)) -> bf16x8 {
+            if (i < NS) {
+                const int ks = i / KB, kb = i % KB;
+                return *reinterpret_cast<const bf16x8*>(kl + (kb * 32 + l32) * L::K_STRIDE +
+                                                        hh * 8 + ks * 16);
+            }
+            const int j = i - NS, kb = j / (2 * CB), h2 = (j / CB) % 2, cb = j % CB;
+            const uint16_t* p =
+                vl + (kb * 32 + 16 * hh + 8 * h2 + tr_row) * L::V_STRIDE + tr_col + cb * 32;
+            const s16x4 lo = lds_read_tr(p);
+            const s16x4 hi = lds_read_tr(p + 4 * L::V_STRIDE);
+            const s16x8 w = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+            return __builtin_bit_cast(bf16x8, w);
+        };
+        float mx = -INFINITY, rs0 = 0.f, rs1 = 0.f;
+        auto pair = [&](int pp) __attribute__((always_inline)) {
+            const int kb = pp / 8, h2 = (pp / 4) % 2, e = 2 * (pp % 4);
+            rounded_pair(__builtin_amdgcn_exp2f(fmaf(s_cur[kb][8 * h2 + e], scale_log2, -m_ref)),
+                         __builtin_amdgcn_exp2f(fmaf(s_cur[kb][8 * h2 + e + 1], scale_log2, -m_ref)),
+                         pb[kb][h2], e, rs0, rs1);
+        };
+        if (!HAS_S) {
+#pragma unroll
+            for (int pp = 0; pp < NPAIR; ++pp) pair(pp);
+        }
+        // causal / ragged-end bound for tile t+1 (MASK_NEXT)
+        const int room = (CAUSAL ? min(Skv - 1, qrow + diag) : Skv - 1) - (t + 1) * BN - 16 * hh;
+        if (HAS_S) {
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) s_nxt[kb][r] = 0.f;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        // Operand ring: slot i consumes fr[i % PF] and then refills the entry
+        // slot i - 1 consumed (an MFMA still reading its operands must not see
+        // them overwritten), so operands arrive PF - 1 slots early.  Each slot
+        // is its own scheduling region (sched_barrier), and an empty asm that
+        // reads and writes the running sums and max keeps the pure arithmetic
+        // of the slot from drifting to the end of the tile.
+        bf16x8 fr[PF];
+        static_for<0, PF - 1>([&](auto ic) __attribute__((always_inline)) {
+            fr[decltype(ic)::value] = fetch(decltype(ic)::value);
+        });
+        static_for<0, NM>([&](auto ic) __attribute__((always_inline)) {
+            constexpr int i = decltype(ic)::value;
+            const bf16x8 a = fr[i % PF];
+            if constexpr (i + PF - 1 < NM) fr[(i + PF - 1) % PF] = fetch(i + PF - 1);
+            if constexpr (i < NS) {
+                constexpr int ks = i / KB, kb = i % KB;
+                s_nxt[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], s_nxt[kb], 0, 0, 0);
+            } else {
+                constexpr int j = i - NS, kb = j / (2 * CB), h2 = (j / CB) % 2, cb = j % CB;
+                oacc[cb] =
+                    __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kb][h2], oacc[cb], 0, 0, 0);
+            }
+            if constexpr (HAS_S) {
+                static_for<0, NPAIR>([&](auto pc) __attribute__((always_inline)) {
+                    constexpr int pp = decltype(pc)::value;
+                    if constexpr (pp * EXP_SLOTS / NPAIR == i) pair(pp);
+                });
+                static_for<0, NMAXV>([&](auto vc) __attribute__((always_inline)) {
+                    constexpr int v = decltype(vc)::value;
+                    if constexpr (MAX0 + v * (NM - MAX0) / NMAXV == i) {
+                        if (MASK_NEXT && (v / 16) * 32 + v % 16 > room)
+                            s_nxt[v / 16][v % 16] = -INFINITY;
+                        mx = fmaxf(mx, s_nxt[v / 16][v % 16]);
+                    }
+                });
+            }
+            if constexpr (HAS_S) asm volatile("" : "+v"(rs0), "+v"(rs1), "+v"(mx));
+            __builtin_amdgcn_sched_barrier(0);
+        });
+        l_i += rs0 + rs1;
+        return HAS_S ? half_swap_max(mx) : -INFINITY;
+    };
+
     // ---- main loop over K/V tiles ------------------------------------------
     // Every schedule runs its tiles in two loops: first the tiles that need no
     // mask, then the masked ones (compile-time tag), so the masking code never
     // sits in the common loop body.
-    auto two_loops = [&](int t0, auto&& step) {
+    auto two_loops = [&](int t0, auto&& step) __attribute__((always_inline)) {
         int t = t0;
         const int split = max(t0, min(first_masked, n_tiles));
         for (; t < split; ++t) step(t, std::false_type{});
         for (; t < n_tiles; ++t) step(t, std::true_type{});
     };
-    u32x4 kr[CH], vr[CH];
     if (PIPE == 0) {
         two_loops(0, [&](int t, auto mask_tag) {
-            load_rows(Kb, t, kr);
-            load_rows(Vb, t, vr);
-            store_k(kslot0, kr);
-            store_v(vslot0, vr);
+            dma_k(t, kslot0);
+            dma_v(t, vslot0);
             __syncthreads();
             if (wave_active(t)) {
                 f32x16 s[KB];
@@ -367,18 +541,16 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
             __syncthreads();
         });
     } else if (PIPE == 1) {
-        // tile t+1 is fetched into registers while tile t is computed from
-        // LDS, then written to the other slot; one barrier per tile
-        load_rows(Kb, 0, kr);
-        load_rows(Vb, 0, vr);
-        store_k(kslot0, kr);
-        store_v(vslot0, vr);
+        // tile t+1 streams into the other slot while tile t is computed from
+        // LDS; one barrier per tile
+        dma_k(0, kslot0);
+        dma_v(0, vslot0);
         __syncthreads();
         two_loops(0, [&](int t, auto mask_tag) {
             const bool odd = t & 1;
             if (t + 1 < n_tiles) {
-                load_rows(Kb, t + 1, kr);
-                load_rows(Vb, t + 1, vr);
+                dma_k(t + 1, odd ? kslot0 : kslot1);
+                dma_v(t + 1, odd ? vslot0 : vslot1);
             }
             if (wave_active(t)) {
                 f32x16 s[KB];
@@ -387,13 +559,9 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
                 probs(s, softmax_stats(s, t, mask_tag), pb);
                 pv(odd ? vslot1 : vslot0, pb);
             }
-            if (t + 1 < n_tiles) {
-                store_k(odd ? kslot0 : kslot1, kr);
-                store_v(odd ? vslot0 : vslot1, vr);
-            }
             __syncthreads();
         });
-    } else {
+    } else if (PIPE == 2) {
         // Ping-pong.  LDS holds K_t, K_{t+1} and V_{t-1}, V_t in two-slot
         // rings (tile t in slot t&1).  Per tile t:
         //   phase 1: A: PV(t-1), S(t)          B: softmax(t)
@@ -401,6 +569,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
         // The global loads of K_{t+2} and V_{t+1} are issued at the start of
         // phase 1 and written to LDS at the end of phase 2 (into the slots of
         // K_t and V_{t-1}, whose last readers finished in phase 1).
+        u32x4 kr[CH], vr[CH];  // tile data staged through registers
         const bool group_b = wave >= 4;
         f32x16 s[KB];
         bf16x8 pb[KB][2];
@@ -447,6 +616,63 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
             __syncthreads();
         });
         if (pv_pending) pv(((n_tiles - 1) & 1) ? vslot1 : vslot0, pb);
+    } else {
+        // Software pipeline.  Iteration t issues the MFMAs of S(t+1) and PV(t)
+        // and, between them in program order, the exponentials of tile t and
+        // the row max of tile t+1: a wave issues in order, so an MFMA followed
+        // by independent VALU instructions keeps the matrix core and the VALU
+        // busy together.  While iteration t runs LDS holds K_{t+1} and V_t,
+        // and K_{t+2} and V_{t+1} stream into the slots of K_t and V_{t-1}
+        // (tile j lives in slot j & 1).
+        // Scores alternate between two register sets (A for even tiles, B for
+        // odd ones), so the loop runs two tiles per trip.
+        f32x16 sA[KB], sB[KB];
+        bf16x8 pb[KB][2];
+        float mx_next = -INFINITY;  // row max of the next tile's scores
+        dma_k(0, kslot0);
+        dma_v(0, vslot0);
+        if (n_tiles > 1) dma_k(1, kslot1);
+        __syncthreads();
+        if (wave_active(0)) {
+            scores(kslot0, sA);
+            mx_next = first_masked <= 0 ? tile_max(sA, 0, std::true_type{})
+                                        : tile_max(sA, 0, std::false_type{});
+        }
+        __syncthreads();  // slot 0 takes K_2 at the end of iteration 0
+
+        // Iteration t.  Its S(t+1) also runs on the last tile, against a stale
+        // but finite K slot, and on a wave's first inactive tile; those scores
+        // are never used.  Keeping S(t+1) unconditional leaves one body per
+        // masking mode.
+        auto iter = [&](int t, f32x16 (&s_cur)[KB], f32x16 (&s_nxt)[KB], auto mask_tag) __attribute__((always_inline)) {
+            const bool odd = t & 1;
+            if (t + 2 < n_tiles) dma_k(t + 2, odd ? kslot1 : kslot0);
+            if (t + 1 < n_tiles) dma_v(t + 1, odd ? vslot0 : vslot1);
+            const uint16_t* const k_next = odd ? kslot0 : kslot1;  // K_{t+1}
+            const uint16_t* const v_cur = odd ? vslot1 : vslot0;   // V_t
+            if (wave_active(t)) {
+                const float m_ref = update_ref(mx_next);
+                mx_next = fused_tile(k_next, v_cur, s_cur, s_nxt, pb, t, m_ref, std::true_type{},
+                                     mask_tag);
+            }
+            __syncthreads();
+        };
+        // Two loops, one per masking mode of the next tile, each running two
+        // tiles per trip (score sets A and B alternate).  The second loop
+        // starts with the current scores in set A.
+        const int split = max(0, min(first_masked - 1, n_tiles));
+        auto run = [&](int t0, int t1, auto mask_tag) __attribute__((always_inline)) {
+            for (int t = t0; t < t1; t += 2) {
+                iter(t, sA, sB, mask_tag);
+                if (t + 1 < t1) iter(t + 1, sB, sA, mask_tag);
+            }
+        };
+        run(0, split, std::false_type{});
+        if (split & 1) {
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb) sA[kb] = sB[kb];
+        }
+        run(split, n_tiles, std::true_type{});
     }
 
     // ---- epilogue: O = O^T / l, one query row per lane ----------------------

@@ -72,11 +72,13 @@ int round_up(int x, int a) { return (x + a - 1) / a * a; }
 // VGPRs per lane of one prefill wave: Q operand (d/4), score accumulators
 // (bn/2), bf16 probabilities (bn/4), output accumulator (d/2), two sets of
 // K and V operands read from LDS, staging registers of the K and V tiles, and
+// (pipe 3) a second set of score accumulators, and
 // scalars/addresses.  Used only when the compiled kernel cannot be queried.
 int fwd_vgprs(int d, int bn, int waves, int pipe) {
     const int nt = waves * 64;
     const int ch = (bn * d / 8 + nt - 1) / nt;
-    int v = d / 4 + bn / 2 + bn / 4 + d / 2 + 2 * (bn / 32) * 4 + 2 * (d / 32) * 4 +
+    int v = d / 4 + (pipe == 3 ? 2 : 1) * bn / 2 + bn / 4 + d / 2 + 2 * (bn / 32) * 4 +
+            2 * (d / 32) * 4 +
             (pipe ? 2 : 1) * ch * 4 + 24;
     return round_up(v, 8);
 }
@@ -112,6 +114,7 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
     // legality: capacities and primitive validity
     if (bn % 32 != 0 || d % 32 != 0) return false;
     if (pipe == 2 && waves != 8) return false;
+    if (pipe == 3 && bn > 64) return false;
     if (p.lds_bytes > desc.lds_bytes_per_cu) return false;
     if (p.vgprs > desc.vgprs_per_simd_lane) return false;
     const int simds = desc.simds_per_cu;

@@ -75,8 +75,8 @@ def test_fwd_small_planned(pa, shape):
     _fwd_case(pa, *shape, seed=10 + sum(shape[:5]))
 
 
-VARIANTS = [(bn, w, pp) for bn in (32, 64, 128) for w in (4, 8) for pp in (0, 1, 2)
-            if pp < 2 or w == 8]
+VARIANTS = [(bn, w, pp) for bn in (32, 64, 128) for w in (4, 8) for pp in (0, 1, 2, 3)
+            if (pp != 2 or w == 8) and (pp != 3 or bn <= 64)]
 
 
 @pytest.mark.parametrize("variant", VARIANTS, ids=[f"bn{a}_w{b}_pipe{c}" for a, b, c in VARIANTS])
