@@ -72,9 +72,12 @@ int attn_fwd(const void* q, const void* k, const void* v, float* o, int B, int H
  *   and the chunk is ceil(Skv / n_splits) keys (empty splits are never
  *   launched).  Every split count gives the same result up to fp32
  *   rounding.
- * Workspace: the library allocates B*H*n*(d+2)*4 bytes stream-ordered from
- * its own memory pool and frees it stream-ordered after the combine; it
- * returns ATTN_ENOMEM if that allocation fails.
+ * Workspace: B*H*n*(d+2)*4 bytes of device memory that the library owns and
+ * keeps per stream, reused by every later call on that stream (stream order
+ * serialises them) until the process ends.  A call that needs more than the
+ * stream's current workspace drains that stream once, frees it and allocates
+ * the next power of two; ATTN_ENOMEM if that allocation fails.  No other
+ * call allocates or synchronises.
  */
 int attn_decode(const void* q, const void* k, const void* v, float* o, int B, int H, int Skv,
                 int d, int n_splits);
@@ -113,6 +116,14 @@ typedef struct attn_device_desc {
     double hbm_bytes_per_s;            /* sustained HBM read bandwidth */
     double hbm_latency_us;             /* loaded HBM latency (for bytes in flight) */
     double launch_us;                  /* kernel launch + drain overhead */
+    /* Offline-calibrated prefill resource model (cycles at clock_ghz), fitted
+     * once per architecture from the block-size ablation
+     * (paper_2609_29219_amd/plan_ablation.py --fit); attn_measure_device()
+     * leaves them unchanged. */
+    double issue_cycles_per_score;     /* non-MFMA issue cycles of a wave per score */
+    double valu_mfma_overlap;          /* share of that hidden behind another wave's MFMAs */
+    double tile_sync_cycles;           /* per K/V tile: barrier and slot hand-off */
+    double tile_latency_cycles;        /* K/V tile load latency exposed without prefetch */
 } attn_device_desc;
 
 /* Fill *out from the current HIP device (structural properties) and the

@@ -58,6 +58,10 @@ class DeviceDesc(ctypes.Structure):
         ("hbm_bytes_per_s", ctypes.c_double),
         ("hbm_latency_us", ctypes.c_double),
         ("launch_us", ctypes.c_double),
+        ("issue_cycles_per_score", ctypes.c_double),
+        ("valu_mfma_overlap", ctypes.c_double),
+        ("tile_sync_cycles", ctypes.c_double),
+        ("tile_latency_cycles", ctypes.c_double),
     ]
 
     def as_dict(self) -> dict:
@@ -71,6 +75,13 @@ def _load() -> ctypes.CDLL:
         raise ImportError(
             f"{LIB_PATH} is not built; run `python paper_2609_29219_amd/build.py` "
             "(or __graft_entry__.build())")
+    # One HIP runtime per process: torch ships its own libamdhip64, and the
+    # library must bind to that one (loaded first, it satisfies the library's
+    # dependency), not load the system copy beside it.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(LIB_PATH)
     vp, ci, cf = ctypes.c_void_p, ctypes.c_int, ctypes.c_float
     lib.attn_fwd.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, cf, ci]
@@ -85,8 +96,11 @@ def _load() -> ctypes.CDLL:
     lib.attn_get_plan.argtypes = [ci, ci, ci, ci, ci, ci, ci, ci, ctypes.c_char_p, ci]
     lib.attn_get_plan_for.argtypes = [ctypes.POINTER(DeviceDesc), ci, ci, ci, ci, ci, ci, ci,
                                       ci, ctypes.c_char_p, ci]
+    lib.attn__fwd_candidates.argtypes = [ctypes.POINTER(DeviceDesc), ci, ci, ci, ci, ci, ci, ci,
+                                         ctypes.c_char_p, ci]
     for fn in (lib.attn_fwd, lib.attn_decode, lib.attn_set_stream, lib.attn_query_device,
-               lib.attn_measure_device, lib.attn_get_plan, lib.attn_get_plan_for):
+               lib.attn_measure_device, lib.attn_get_plan, lib.attn_get_plan_for,
+               lib.attn__fwd_candidates):
         fn.restype = ci
     return lib
 
@@ -178,6 +192,21 @@ def get_plan(kind: int, B: int, H: int, Sq: int, Skv: int, d: int, causal: bool 
     if rc < 0:
         raise AttnError(rc, last_error())
     return buf.value.decode()
+
+
+def fwd_candidates(B: int, H: int, Sq: int, Skv: int, d: int, causal: bool = False,
+                   desc: DeviceDesc | None = None, device_footprint: bool = False) -> list[dict]:
+    """Every feasible prefill candidate with its modelled time (not ABI; for
+    the block-size ablation).  desc None: this device's description and the
+    compiled kernels' real register/occupancy footprint; with a desc, the
+    footprint is estimated unless device_footprint is set."""
+    buf = ctypes.create_string_buffer(1 << 16)
+    ptr = ctypes.byref(desc) if desc is not None else None
+    rc = lib.attn__fwd_candidates(ptr, B, H, Sq, Skv, d, int(bool(causal)),
+                                  int(bool(device_footprint)), buf, 1 << 16)
+    if rc < 0:
+        raise AttnError(rc, last_error())
+    return [parse_plan(l) for l in buf.value.decode().splitlines() if l.strip()]
 
 
 def parse_plan(line: str) -> dict:

@@ -7,6 +7,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
 #include <map>
 #include <mutex>
 #include <string>
@@ -81,11 +82,20 @@ int fail_hip(hipError_t e, const char* what) {
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 // ---- per-device state --------------------------------------------------
+// The decode workspace is cached per stream and reused by every later call on
+// that stream (stream order serialises them).  Stream-ordered pool
+// allocation (hipMallocFromPoolAsync / hipFreeAsync) blocks the host until
+// the previous call's free has executed on this runtime, so it would turn
+// every decode call into a synchronisation.
+struct Workspace {
+    void* ptr = nullptr;
+    size_t bytes = 0;
+};
 struct DeviceState {
     bool ready = false;
     bool is_gfx950 = false;
     attn_device_desc desc{};
-    hipMemPool_t pool = nullptr;
+    std::map<hipStream_t, Workspace> ws;
 };
 std::mutex g_mu;
 std::map<int, DeviceState> g_devices;
@@ -204,8 +214,10 @@ int attn_get_plan_for(const attn_device_desc* desc, int kind, int B, int H, int 
         desc->mfma_bf16_flops_per_clk_cu <= 0.0 || desc->lds_bytes_per_clk_cu <= 0.0 ||
         desc->l2_bytes_per_clk_xcd <= 0.0 || desc->valu_lanes_per_clk_simd <= 0.0 ||
         desc->simds_per_cu <= 0 || desc->wave_size <= 0 || desc->vgprs_per_simd_lane <= 0 ||
-        desc->max_waves_per_simd <= 0)
-        return fail(ATTN_EINVAL, "device description has non-positive fields");
+        desc->max_waves_per_simd <= 0 || desc->issue_cycles_per_score < 0.0 ||
+        desc->valu_mfma_overlap < 0.0 || desc->valu_mfma_overlap >= 1.0 ||
+        desc->tile_sync_cycles < 0.0 || desc->tile_latency_cycles < 0.0)
+        return fail(ATTN_EINVAL, "device description has out-of-range fields");
     if (kind == ATTN_KIND_FWD) {
         if (causal && Sq > Skv) return fail(ATTN_EUNSUPPORTED, "causal needs Sq <= Skv");
         FwdPlan p;
@@ -220,6 +232,39 @@ int attn_get_plan_for(const attn_device_desc* desc, int kind, int B, int H, int 
         return format_decode_plan(p, buf, buflen);
     }
     return fail(ATTN_EINVAL, "unknown plan kind %d", kind);
+}
+
+// Not part of the ABI: every feasible prefill candidate with its modelled
+// time, one plan line each (newline-separated), for the block-size ablation
+// that validates the model (plan_ablation.py).  Returns the full length.
+// device_footprint != 0: with a gfx950 device present, use the compiled
+// kernels' real register and occupancy footprint (always so for desc NULL);
+// otherwise the estimate, as attn_get_plan_for does for an explicit desc.
+int attn__fwd_candidates(const attn_device_desc* desc, int B, int H, int Sq, int Skv, int d,
+                         int causal, int device_footprint, char* buf, int buflen) {
+    attn_device_desc local;
+    FwdResFn res = nullptr;
+    const bool have = attn_query_device(&local) == ATTN_OK && strcmp(local.arch, "gfx950") == 0;
+    if (have && (device_footprint || !desc)) res = fwd_resources;
+    if (!desc) desc = &local;
+    if (buflen < 0 || (buflen > 0 && !buf)) return fail(ATTN_EINVAL, "bad output buffer");
+    if (B <= 0 || H <= 0 || Sq <= 0 || Skv <= 0) return fail(ATTN_EINVAL, "bad dimensions");
+    if (d != 64 && d != 128) return fail(ATTN_EUNSUPPORTED, "head dim %d not in {64, 128}", d);
+    FwdPlan plans[64];
+    const int n = std::min(64, plan_fwd_all(*desc, B, H, Sq, Skv, d, causal ? 1 : 0, plans, 64, res));
+    int len = 0;
+    for (int i = 0; i < n; ++i) {
+        char line[512];
+        const int l = format_fwd_plan(plans[i], line, sizeof line);
+        if (buf && len + l + 1 < buflen) {
+            memcpy(buf + len, line, l);
+            buf[len + l] = '\n';
+            buf[len + l + 1] = '\0';
+        }
+        len += l + 1;
+    }
+    if (buf && buflen > 0 && len >= buflen) buf[buflen - 1] = '\0';
+    return len;
 }
 
 int attn_get_plan(int kind, int B, int H, int Sq, int Skv, int d, int causal, int n_splits,
@@ -282,36 +327,38 @@ int attn_decode(const void* q, const void* k, const void* v, float* o, int B, in
                 return fail(ATTN_EUNSUPPORTED, "no feasible decode plan for this shape");
             g_dec_cache[key] = plan;
         }
-        if (!st->pool) {
-            int dev = 0;
-            hipGetDevice(&dev);
-            hipMemPoolProps props;
-            memset(&props, 0, sizeof props);
-            props.allocType = hipMemAllocationTypePinned;
-            props.location.type = hipMemLocationTypeDevice;
-            props.location.id = dev;
-            hipError_t e = hipMemPoolCreate(&st->pool, &props);
-            if (e != hipSuccess) {
-                st->pool = nullptr;
-                return fail_hip(e, "hipMemPoolCreate");
-            }
-            uint64_t keep = UINT64_MAX;  // keep freed blocks for reuse
-            hipMemPoolSetAttribute(st->pool, hipMemPoolAttrReleaseThreshold, &keep);
-        }
     }
     const size_t ws_bytes = (size_t)B * H * plan.n_splits * (d + 2) * sizeof(float);
     void* ws = nullptr;
-    hipError_t e = hipMallocFromPoolAsync(&ws, ws_bytes, st->pool, t_stream);
-    if (e != hipSuccess || !ws) {
-        (void)hipGetLastError();
-        return fail(ATTN_ENOMEM, "decode workspace of %zu bytes: %s", ws_bytes,
-                    hipGetErrorString(e));
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        Workspace& w = st->ws[t_stream];
+        if (w.bytes < ws_bytes) {
+            // grow to the next power of two; the old buffer may still be in use
+            // by work queued on this stream, so drain the stream first (rare)
+            size_t want = 4096;
+            while (want < ws_bytes) want *= 2;
+            if (w.ptr) {
+                hipError_t e = hipStreamSynchronize(t_stream);
+                if (e == hipSuccess) e = hipFree(w.ptr);
+                if (e != hipSuccess) return fail_hip(e, "decode workspace release");
+                w = Workspace{};
+            }
+            hipError_t e = hipMalloc(&w.ptr, want);
+            if (e != hipSuccess || !w.ptr) {
+                (void)hipGetLastError();
+                w = Workspace{};
+                return fail(ATTN_ENOMEM, "decode workspace of %zu bytes: %s", want,
+                            hipGetErrorString(e));
+            }
+            w.bytes = want;
+        }
+        ws = w.ptr;
     }
     const float scale = (float)(1.0 / sqrt((double)d));
-    e = launch_decode(plan, q, k, v, o, static_cast<float*>(ws), B, H, Skv, scale, t_stream);
-    hipError_t e2 = hipFreeAsync(ws, t_stream);
+    const hipError_t e =
+        launch_decode(plan, q, k, v, o, static_cast<float*>(ws), B, H, Skv, scale, t_stream);
     if (e != hipSuccess) return fail_hip(e, "decode launch");
-    if (e2 != hipSuccess) return fail_hip(e2, "decode workspace free");
     return ATTN_OK;
 }
 

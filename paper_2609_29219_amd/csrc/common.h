@@ -71,6 +71,10 @@ bool plan_fwd(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d
 bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d,
                     int causal, int bn, int waves, int pipe, FwdPlan* out,
                     FwdResFn res = nullptr);
+// Every feasible candidate (in the planner's search order), up to cap of them
+// into out; returns how many there are.
+int plan_fwd_all(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d, int causal,
+                 FwdPlan* out, int cap, FwdResFn res = nullptr);
 bool fwd_resources(int d, int bn, int waves, int pipe, int causal, KernelRes* out);
 bool plan_decode(const attn_device_desc& desc, int B, int H, int Skv, int d, int n_splits,
                  DecodePlan* out);

@@ -153,7 +153,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: scalar
     const int l32 = lane & 31;
     const int hh = lane >> 5;
 
@@ -177,23 +177,28 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     const uint16_t* Kb = K + kv_base;
     const uint16_t* Vb = V + kv_base;
 
-    for (int pass = 0; pass < n_pass; ++pass) {
-    const int qt = CAUSAL ? (pass == 0 ? n_qtiles - 1 - unit : unit) : unit;
-    const int q_wave0 = qt * BM + wave * 32;  // first query row of this wave
-    const int qrow = q_wave0 + l32;
-
-    // ---- Q tile into VGPRs, as the B operand (16 dims x 32 queries) --------
+    auto qt_of = [&](int pass) __attribute__((always_inline)) {
+        return CAUSAL ? (pass == 0 ? n_qtiles - 1 - unit : unit) : unit;
+    };
+    // ---- Q tile into VGPRs, as the B operand (16 dims x 32 queries) ----------
     bf16x8 qf[KD];
-    {
+    auto load_q = [&](int qt) __attribute__((always_inline)) {
         // rows past Sq read the last row (finite data; never stored)
-        const uint16_t* qp = Q + ((long long)bh * Sq + min(qrow, Sq - 1)) * D + hh * 8;
+        const int row = min(qt * BM + wave * 32 + l32, Sq - 1);
+        const uint16_t* qp = Q + ((long long)bh * Sq + row) * D + hh * 8;
 #pragma unroll
         for (int ks = 0; ks < KD; ++ks) {
             u32x4 w = *reinterpret_cast<const u32x4*>(qp + ks * 16);
             w ^= q_sign;  // exact negation for a negative scale
             qf[ks] = __builtin_bit_cast(bf16x8, w);
         }
-    }
+    };
+    load_q(qt_of(0));
+
+    for (int pass = 0; pass < n_pass; ++pass) {
+    const int qt = qt_of(pass);
+    const int q_wave0 = qt * BM + wave * 32;  // first query row of this wave
+    const int qrow = q_wave0 + l32;
 
     // ---- key range of this workgroup ------------------------------------
     int kv_end = Skv;
@@ -204,9 +209,11 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     const int n_tiles = (kv_end + BN - 1) / BN;
     // causal: a tile entirely above this wave's diagonal is skipped
     auto wave_active = [&](int t) __attribute__((always_inline)) { return !CAUSAL || t * BN <= q_wave0 + 31 + diag; };
-    // tiles before first_masked need no mask for any row of this workgroup
+    // tiles before first_masked need no mask for any row of this wave.  The
+    // split is per wave (on the diagonal, the waves of lower rows start
+    // masking earlier); every wave still runs one barrier per tile.
     int first_masked = Skv / BN;  // the ragged tail tile, if any
-    if (CAUSAL) first_masked = min(first_masked, (qt * BM + diag + 1) / BN);
+    if (CAUSAL) first_masked = min(first_masked, (q_wave0 + diag + 1) / BN);
 
     // Rows past the end of the key range are loaded from the last valid row
     // (clamped, never out of bounds): their scores are masked to weight 0,
@@ -245,51 +252,67 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
         }
     };
 
-    // Direct global -> LDS tile loads (pipes 0, 1, 3).  global_load_lds_dwordx4
-    // writes lane i's 16 bytes at the wave-uniform LDS base + 16*i, so a tile
-    // region (its padded rows laid end to end) is filled in 1 KiB pieces, and
-    // each lane picks the source chunk that belongs at its position: the K row
-    // permutation and the padding live in the source addresses (a padding
-    // position re-reads a chunk of its own row).  No registers carry tile
-    // data, and the loads complete behind the barrier that publishes them.
+    // Direct global -> LDS tile loads (pipes 0, 1, 3) with buffer_load ... lds:
+    // lane i of an instruction writes its 16 bytes at the wave-uniform LDS base
+    // + 16*i, so a tile region (its padded rows laid end to end) is filled in
+    // 1 KiB pieces, and each lane picks the source chunk that belongs at its
+    // position: the K row permutation and the padding live in the source
+    // offsets (a padding position re-reads a chunk of its own row).  The
+    // buffer resource holds this head's K or V slab (reads past it return 0),
+    // the tile base is a scalar offset and each lane's offset within the tile
+    // is fixed, so issuing a tile costs no vector arithmetic and no registers
+    // carry tile data; the loads complete behind the barrier that publishes
+    // them.
     constexpr int DCH = D / 8;                                   // 16-byte chunks of a row
     constexpr int KST = L::K_STRIDE / 8, VST = L::V_STRIDE / 8;  // per padded LDS row
     constexpr int KCH = BN * KST, VCH = BN * VST;                // positions per region
     constexpr int KI = (KCH + 63) / 64, VI = (VCH + 63) / 64;    // pieces per region
-    constexpr int KJ = (KI + NW - 1) / NW, VJ = (VI + NW - 1) / NW;  // pieces per wave
-    // element offset of this lane's source chunk inside a tile, -1 for none
-    int koff[KJ], voff[VJ];
+    constexpr int NJ = (KI + VI + NW - 1) / NW;  // pieces per wave (K pieces, then V)
+    constexpr int kRsrcFlags = 0x00020000;       // raw 32-bit buffer, gfx9 family
+    const int slab_bytes = Skv * D * 2;          // fits in 31 bits (checked by the host)
+    const __amdgpu_buffer_rsrc_t k_rsrc =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(Kb), 0, slab_bytes, kRsrcFlags);
+    const __amdgpu_buffer_rsrc_t v_rsrc =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(Vb), 0, slab_bytes, kRsrcFlags);
+    // Piece p (0 <= p < KI + VI) goes to wave p % NW: K pieces first, then V.
+    // off[j]: byte offset inside a tile of this lane's source chunk for the
+    // wave's j-th piece, -1 for none.
+    int off[NJ];
 #pragma unroll
-    for (int j = 0; j < KJ; ++j) {
-        const int i = wave + j * NW, pos = i * 64 + lane;
-        const int prow = pos / KST, key = (prow & ~31) | (16 * ((prow & 7) >> 2) +
-                                                          4 * ((prow & 31) >> 3) + (prow & 3));
-        koff[j] = (i < KI && pos < KCH) ? key * D + min(pos % KST, DCH - 1) * 8 : -1;
+    for (int j = 0; j < NJ; ++j) {
+        const int piece = wave + j * NW;
+        const bool is_k = piece < KI;
+        const int i = is_k ? piece : piece - KI, pos = i * 64 + lane;
+        const int st = is_k ? KST : VST;
+        const int prow = pos / st, c = min(pos % st, DCH - 1);
+        const int key = is_k ? (prow & ~31) | (16 * ((prow & 7) >> 2) + 4 * ((prow & 31) >> 3) +
+                                              (prow & 3))
+                             : prow;
+        const bool ok = piece < KI + VI && pos < (is_k ? KCH : VCH);
+        off[j] = ok ? (key * D + c * 8) * 2 : -1;
     }
+    // Issue this wave's pieces of K tile tk (into kdst) and/or V tile tv
+    // (into vdst); a negative tile index skips that operand.
+    auto dma = [&](int tk, uint16_t* kdst, int tv, uint16_t* vdst) __attribute__((always_inline)) {
 #pragma unroll
-    for (int j = 0; j < VJ; ++j) {
-        const int i = wave + j * NW, pos = i * 64 + lane;
-        voff[j] = (i < VI && pos < VCH) ? (pos / VST) * D + min(pos % VST, DCH - 1) * 8 : -1;
-    }
-    auto dma_tile = [&](const uint16_t* base, int t, uint16_t* dst, const int* off, int nj,
-                        int ni) __attribute__((always_inline)) {
-        const int key0 = t * BN;
-        const bool ragged = key0 + BN > Skv;  // rows past the end re-read the last key
-        const uint16_t* tb = base + (long long)key0 * D;
-        for (int j = 0; j < nj; ++j) {
-            const int i = wave + j * NW;
-            if (i < ni && off[j] >= 0) {
-                int o = off[j];
-                if (ragged) o = (min(key0 + o / D, Skv - 1) - key0) * D + o % D;
-                __builtin_amdgcn_global_load_lds(tb + o, dst + i * 512, 16, 0, 0);
-            }
+        for (int j = 0; j < NJ; ++j) {
+            const int piece = wave + j * NW;
+            if (piece >= KI + VI) continue;
+            const bool is_k = piece < KI;
+            const int t = is_k ? tk : tv;
+            if (t < 0 || off[j] < 0) continue;
+            const int key0 = t * BN;
+            int o = off[j];
+            if (key0 + BN > Skv)  // ragged tile: rows past the end re-read the last key
+                o = ((min(key0 + o / (2 * D), Skv - 1) - key0) * D) * 2 + o % (2 * D);
+            uint16_t* dst = is_k ? kdst + piece * 512 : vdst + (piece - KI) * 512;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                is_k ? k_rsrc : v_rsrc, (__attribute__((address_space(3))) void*)dst, 16, o,
+                key0 * D * 2, 0, 0);
         }
     };
     auto dma_k = [&](int t, uint16_t* dst) __attribute__((always_inline)) {
-        dma_tile(Kb, t, dst, koff, KJ, KI);
-    };
-    auto dma_v = [&](int t, uint16_t* dst) __attribute__((always_inline)) {
-        dma_tile(Vb, t, dst, voff, VJ, VI);
+        dma(t, dst, -1, dst);  // the V destination is unused
     };
 
     // ---- online-softmax state (one query row per lane) --------------------
@@ -429,7 +452,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
         constexpr int NS = HAS_S ? KB * KD : 0;  // MFMAs of S(t+1)
         constexpr int NPV = KB * 2 * CB;          // MFMAs of PV(t)
         constexpr int NM = NS + NPV;
-        constexpr int PF = 3;
+        constexpr int PF = CAUSAL ? 2 : 3;  // causal needs the registers
         constexpr int NPAIR = KB * 8;                    // pairs of probabilities per lane
         constexpr int EXP_SLOTS = HAS_S ? NS + NPV / 2 : 0;  // slots carrying exponentials
         constexpr int MAX0 = EXP_SLOTS + 1;              // first slot carrying the next max
@@ -528,8 +551,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     };
     if (PIPE == 0) {
         two_loops(0, [&](int t, auto mask_tag) {
-            dma_k(t, kslot0);
-            dma_v(t, vslot0);
+            dma(t, kslot0, t, vslot0);
             __syncthreads();
             if (wave_active(t)) {
                 f32x16 s[KB];
@@ -543,15 +565,11 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     } else if (PIPE == 1) {
         // tile t+1 streams into the other slot while tile t is computed from
         // LDS; one barrier per tile
-        dma_k(0, kslot0);
-        dma_v(0, vslot0);
+        dma(0, kslot0, 0, vslot0);
         __syncthreads();
         two_loops(0, [&](int t, auto mask_tag) {
             const bool odd = t & 1;
-            if (t + 1 < n_tiles) {
-                dma_k(t + 1, odd ? kslot0 : kslot1);
-                dma_v(t + 1, odd ? vslot0 : vslot1);
-            }
+            if (t + 1 < n_tiles) dma(t + 1, odd ? kslot0 : kslot1, t + 1, odd ? vslot0 : vslot1);
             if (wave_active(t)) {
                 f32x16 s[KB];
                 bf16x8 pb[KB][2];
@@ -570,7 +588,10 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
         // phase 1 and written to LDS at the end of phase 2 (into the slots of
         // K_t and V_{t-1}, whose last readers finished in phase 1).
         u32x4 kr[CH], vr[CH];  // tile data staged through registers
-        const bool group_b = wave >= 4;
+        // from the thread id, not the scalar wave index: the two groups' bodies
+        // then stay exec-masked regions, which the register allocator handles
+        // far better here than two scalar branches
+        const bool group_b = (tid >> 6) >= 4;
         f32x16 s[KB];
         bf16x8 pb[KB][2];
         bool pv_pending = false;  // group A: PV of the previous tile is due
@@ -629,8 +650,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
         f32x16 sA[KB], sB[KB];
         bf16x8 pb[KB][2];
         float mx_next = -INFINITY;  // row max of the next tile's scores
-        dma_k(0, kslot0);
-        dma_v(0, vslot0);
+        dma(0, kslot0, 0, vslot0);
         if (n_tiles > 1) dma_k(1, kslot1);
         __syncthreads();
         if (wave_active(0)) {
@@ -646,8 +666,8 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
         // masking mode.
         auto iter = [&](int t, f32x16 (&s_cur)[KB], f32x16 (&s_nxt)[KB], auto mask_tag) __attribute__((always_inline)) {
             const bool odd = t & 1;
-            if (t + 2 < n_tiles) dma_k(t + 2, odd ? kslot1 : kslot0);
-            if (t + 1 < n_tiles) dma_v(t + 1, odd ? vslot0 : vslot1);
+            dma(t + 2 < n_tiles ? t + 2 : -1, odd ? kslot1 : kslot0,
+                t + 1 < n_tiles ? t + 1 : -1, odd ? vslot0 : vslot1);
             const uint16_t* const k_next = odd ? kslot0 : kslot1;  // K_{t+1}
             const uint16_t* const v_cur = odd ? vslot1 : vslot0;   // V_t
             if (wave_active(t)) {
@@ -675,6 +695,12 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
         run(split, n_tiles, std::true_type{});
     }
 
+    // The next q-tile's Q is fetched before this one's output is stored, so
+    // waiting for it does not wait for the stores (memory operations of a wave
+    // complete in issue order).
+    if (pass + 1 < n_pass) load_q(qt_of(pass + 1));
+    __builtin_amdgcn_sched_barrier(0);
+
     // ---- epilogue: O = O^T / l, one query row per lane ----------------------
     const float inv = 1.f / half_swap_sum(l_i);
     if (qrow < Sq) {
@@ -688,7 +714,10 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
                 *reinterpret_cast<float4*>(orow + cb * 32 + 8 * g) = val;
             }
     }
-    __syncthreads();  // the next q-tile refills LDS slots read above
+    // Pipes 0, 1 and 3 end every tile with a barrier, after which no wave
+    // reads LDS, so the next q-tile may refill the slots at once; the
+    // ping-pong schedule reads V once more after its last barrier.
+    if (PIPE == 2) __syncthreads();
     }  // pass
 }
 

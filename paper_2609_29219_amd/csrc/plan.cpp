@@ -43,15 +43,24 @@ void default_desc(attn_device_desc* d) {
     d->vgprs_per_simd_lane = 512;
     d->max_waves_per_simd = 8;
     d->clock_ghz = 2.4;
-    // performance properties (per-CU primitive rates)
-    d->mfma_bf16_flops_per_clk_cu = 4096.0;  // 32x32x16 bf16 MFMA: 32 cycles per SIMD
-    d->valu_lanes_per_clk_simd = 16.0;       // a wave64 fp32 op occupies 4 cycles
-    d->trans_cycles_per_op = 16.0;           // a wave64 v_exp_f32 occupies 16 cycles
-    d->lds_bytes_per_clk_cu = 128.0;
+    // performance properties (per-CU primitive rates), as the isolated
+    // microbenchmarks of attn_measure_device() measured them on MI355X, in
+    // cycles of the nominal clock (the MFMA-bound clock is lower, so the MFMA
+    // rate reads below the 4096 flop/clk of the specification)
+    d->mfma_bf16_flops_per_clk_cu = 3452.0;
+    d->valu_lanes_per_clk_simd = 13.8;
+    d->trans_cycles_per_op = 11.9;           // one wave64 v_exp_f32
+    d->lds_bytes_per_clk_cu = 138.0;
     d->l2_bytes_per_clk_xcd = 2048.0;
-    d->hbm_bytes_per_s = 6.0e12;             // sustained stream read
+    d->hbm_bytes_per_s = 5.95e12;            // sustained stream read
     d->hbm_latency_us = 2.0;
     d->launch_us = 4.0;
+    // prefill resource model, calibrated offline on MI355X (plan_ablation.py
+    // --fit over B1 H32 S8192 d128 and causal B2 H16 S4096 d128)
+    d->issue_cycles_per_score = 87.0;
+    d->valu_mfma_overlap = 0.56;
+    d->tile_sync_cycles = 234.0;
+    d->tile_latency_cycles = 687.0;
 }
 
 // HEG composition rules: a pipe node with load, body and store stages and
@@ -70,36 +79,37 @@ namespace {
 int round_up(int x, int a) { return (x + a - 1) / a * a; }
 
 // VGPRs per lane of one prefill wave: Q operand (d/4), score accumulators
-// (bn/2), bf16 probabilities (bn/4), output accumulator (d/2), two sets of
-// K and V operands read from LDS, staging registers of the K and V tiles, and
-// (pipe 3) a second set of score accumulators, and
-// scalars/addresses.  Used only when the compiled kernel cannot be queried.
+// (bn/2; two sets with pipe 3), bf16 probabilities (bn/4), output accumulator
+// (d/2), LDS operands in flight (bn/8, plus a deeper ring with pipe 3), one
+// source offset per 1 KiB LDS piece the wave loads, staging registers of the
+// K and V tiles (pipe 2 only), and scalars/addresses.  Fitted to the compiled
+// variants; used only when the compiled kernel cannot be queried.
 int fwd_vgprs(int d, int bn, int waves, int pipe) {
     const int nt = waves * 64;
     const int ch = (bn * d / 8 + nt - 1) / nt;
-    int v = d / 4 + (pipe == 3 ? 2 : 1) * bn / 2 + bn / 4 + d / 2 + 2 * (bn / 32) * 4 +
-            2 * (d / 32) * 4 +
-            (pipe ? 2 : 1) * ch * 4 + 24;
+    const int pieces = (bn * ((d + 8) / 8 + (d + 32) / 8) + 63) / 64;
+    const int per_wave = (pieces + waves - 1) / waves;
+    int v = d / 4 + (pipe == 3 ? 2 : 1) * bn / 2 + bn / 4 + d / 2 + 28 + bn / 8 + per_wave +
+            (pipe == 2 ? 2 * ch * 4 : 0) + (pipe == 3 ? 12 : 0);
     return round_up(v, 8);
 }
 
 }  // namespace
 
-// Prefill model.  Per wave and K/V tile of BN keys:
-//   M  = MFMA cycles: 2*(BN/32)*(D/16) v_mfma_f32_32x32x16_bf16 (S and PV)
-//   V  = VALU cycles: per score one FMA, one v_exp, and a half each of
-//        v_max3, v_cvt_pk_bf16_f32 and v_dot2c (32*BN/64 scores per lane),
-//        plus a fixed part (max exchange, bookkeeping)
-//   LDS: 4*BN*D bytes read per wave (K and V operands)
-// A wave does not issue VALU work while its own MFMAs execute, but two waves
-// sharing a SIMD overlap.  Waves of one workgroup run in lockstep between
-// barriers (same phase), so with w waves per SIMD from g independent
-// workgroups the tile-round costs w*M + w*V minus the overlap
-// ((g-1)/g)*min(w*M, w*V); the ping-pong pipe (2) runs its wave pairs in
-// opposite phases, so each pair costs 2*max(M, V).  LDS bandwidth is shared
-// by the CU.  Loads of the next tile overlap compute when the pipe knob opens
-// the load/body boundary (pipe >= 1); with pipe 0 the load latency is
-// exposed to the workgroup, hidden by the other resident workgroups.
+// Prefill model (cycles of the nominal clock).  Per wave and K/V tile of BN
+// keys:
+//   M = MFMA cycles: 2*(BN/32)*(D/16) v_mfma_f32_32x32x16_bf16 (S and PV)
+//   V = non-MFMA issue cycles: issue_cycles_per_score per score, 32*BN/64
+//       scores per lane (softmax VALU, conversions, operand waits)
+// With w waves per SIMD (from g resident workgroups of NW waves), a share
+// valu_mfma_overlap of V hides behind other waves' MFMAs (none with one wave
+// per SIMD), and every workgroup pays tile_sync_cycles per tile:
+//   body = g * ((NW/4) * (M + (1 - overlap) * V) + sync)    [ping-pong: 2 syncs]
+// LDS bandwidth bounds it from below (K/V operand reads of every wave plus
+// the tile writes).  The tile load is a pipe node (load, body, -) whose
+// load/body boundary the pipe knob opens (pipe >= 1, Eq. heg-pipe): with pipe
+// 0 the load latency is exposed, shared by the g resident workgroups.  A
+// q-tile adds one exposed latency (Q and the first tile) to its loop.
 bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d,
                     int causal, int bn, int waves, int pipe, FwdPlan* out, FwdResFn res) {
     FwdPlan p;
@@ -136,33 +146,21 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
     p.grid = (long long)B * H * (causal ? (p.n_qtiles + 1) / 2 : p.n_qtiles);
     if (p.grid > 0x7fffffffLL) return false;
 
-    const double bm = p.block_m;
-    const int cus_per_xcd = std::max(1, desc.num_cus / std::max(1, desc.num_xcds));
-    const double l2_share = desc.l2_bytes_per_clk_xcd / cus_per_xcd;  // bytes/clk per CU
     const double mfma_cyc = 32768.0 / (desc.mfma_bf16_flops_per_clk_cu / simds);
-    const double valu_op = desc.wave_size / desc.valu_lanes_per_clk_simd;  // cycles per op
     const double scores_per_lane = 32.0 * bn / desc.wave_size;
     // ---- primitive costs of one K/V tile -------------------------------
     const double M = 2.0 * (bn / 32) * (d / 16) * mfma_cyc;
-    const double V = scores_per_lane * (2.5 * valu_op + desc.trans_cycles_per_op) + 40.0 * valu_op;
-    const double w = (double)wg * waves / simds;  // waves per SIMD
-    double compute;
-    if (pipe == 2) {
-        compute = w * std::max(M, V);
-    } else {
-        const double g = wg;
-        compute = w * (M + V) - (g - 1.0) / g * std::min(w * M, w * V);
-    }
-    const double lds = wg * waves * 4.0 * bn * d / desc.lds_bytes_per_clk_cu;
-    const double load = wg * 4.0 * bn * d / l2_share;  // K/V tile from L2
-    const double latency = desc.hbm_latency_us * 0.25 * desc.clock_ghz * 1e3;  // L2 hit
+    const double V = scores_per_lane * desc.issue_cycles_per_score;
+    const double wpw = waves / (double)simds;  // waves of one workgroup per SIMD
+    const double overlap = wg * wpw >= 2.0 ? desc.valu_mfma_overlap : 0.0;
+    const double syncs = pipe == 2 ? 2.0 : 1.0;
+    const double compute = wg * (wpw * (M + (1.0 - overlap) * V) + syncs * desc.tile_sync_cycles);
+    const double lds = wg * (waves * 4.0 * bn * d + 4.0 * bn * d) / desc.lds_bytes_per_clk_cu;
     const double body = std::max(compute, lds);
+    const double latency = desc.tile_latency_cycles;
     // pipe node (load, body, -): knob b_lm open for pipe >= 1
-    double tile = heg_pipe(load, body, 0.0, pipe >= 1 ? 1 : 0, 0);
-    if (pipe == 0) tile += latency / wg;  // exposed, shared by the resident workgroups
-    if (pipe == 2) tile += latency / 4;   // second barrier per tile
-    const double load_q = wg * bm * d * 2.0 / l2_share + load + latency;
-    const double store_o = wg * bm * d * 4.0 / l2_share;
+    const double tile = heg_pipe(latency / wg, body, 0.0, pipe >= 1 ? 1 : 0, 0);
+    const double load_q = latency;
 
     // ---- grid: regular (non-causal) or regularised (causal) --------------
     const double slots = (double)desc.num_cus * wg;
@@ -170,7 +168,7 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
     double cycles;
     if (!causal) {
         const double rounds = ceil((double)p.grid / slots);
-        cycles = rounds * (load_q + heg_for(full_tiles, tile) + store_o);
+        cycles = rounds * (load_q + heg_for(full_tiles, tile));
     } else {
         // workgroups take q-tile pairs (n-1-u, u), which regularises the
         // triangular work: per workgroup the sum of the pair's tile counts
@@ -183,8 +181,8 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
         const int units = (p.n_qtiles + 1) / 2;
         for (int u = 0; u < units; ++u) {
             const int heavy = p.n_qtiles - 1 - u;
-            double t = load_q + store_o + heg_for(tiles_of(heavy), tile);
-            if (heavy != u) t += load_q + store_o + heg_for(tiles_of(u), tile);
+            double t = load_q + heg_for(tiles_of(heavy), tile);
+            if (heavy != u) t += load_q + heg_for(tiles_of(u), tile);
             sum += t;
             longest = std::max(longest, t);
         }
@@ -198,11 +196,11 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
     if (hbm_us > us) {
         us = hbm_us;
         bound = "hbm";
-    } else if (pipe >= 1 && load > body) {
-        bound = "l2";
     } else if (lds > compute) {
         bound = "lds";
-    } else if (w * M >= w * V) {
+    } else if (pipe == 0 && wg == 1) {
+        bound = "latency";
+    } else if (wpw * M >= wpw * (1.0 - overlap) * V) {
         bound = "mfma";
     } else {
         bound = "valu";
@@ -231,6 +229,21 @@ bool plan_fwd(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d
             }
     if (found) *out = best;
     return found;
+}
+
+int plan_fwd_all(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d, int causal,
+                 FwdPlan* out, int cap, FwdResFn res) {
+    int n = 0;
+    for (int bn : kFwdBlockN)
+        for (int waves : kFwdWaves)
+            for (int pipe : kFwdPipe) {
+                FwdPlan p;
+                if (!plan_fwd_fixed(desc, B, H, Sq, Skv, d, causal, bn, waves, pipe, &p, res))
+                    continue;
+                if (n < cap) out[n] = p;
+                ++n;
+            }
+    return n;
 }
 
 bool plan_decode(const attn_device_desc& desc, int B, int H, int Skv, int d, int n_req,

@@ -1,0 +1,227 @@
+"""Planner validation on the device: the block-size ablation.
+
+    python paper_2609_29219_amd/plan_ablation.py [--save FILE] [--load FILE] [--fit]
+                                                 [--markdown FILE]
+
+For each workload every feasible prefill candidate (block sizes, waves,
+pipeline knob) is run through the ATTN_FORCE_PLAN hook and timed, and set
+against the planner's modelled time: where the planner's pick ranks among the
+measured times, how far it is from the measured best, whether the best is in
+the modelled top five, the rank correlation of modelled and measured times,
+and the pick's rank among its legal one-step neighbours (block width one
+step up or down, the other wave count, the neighbouring pipeline knob).  The
+paper validates its model the same way (top-k candidates and block-size
+neighbourhoods); measurement here validates, it never selects.
+
+--fit refits the four offline-calibrated fields of the device description
+(issue_cycles_per_score, valu_mfma_overlap, tile_sync_cycles,
+tile_latency_cycles) to the measured times by least squares on log time,
+using the library's own model (the calibration is done once per
+architecture and then frozen into the built-in description).  --load reuses
+a saved measurement instead of timing; the candidates' register and
+occupancy footprint still comes from the compiled kernels on the device.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import math
+import os
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import paper_2609_29219_amd as pa  # noqa: E402
+
+# (name, B, H, Sq, Skv, d, causal)
+WORKLOADS = [
+    ("b1_h32_s8192_d128", 1, 32, 8192, 8192, 128, False),
+    ("b2_h16_s4096_d128_causal", 2, 16, 4096, 4096, 128, True),
+    ("b4_h16_s2048_d128_causal", 4, 16, 2048, 2048, 128, True),
+    ("b4_h16_s2048_d64", 4, 16, 2048, 2048, 64, False),
+    ("b8_h8_s1024_d128", 8, 8, 1024, 1024, 128, False),
+]
+CALIBRATED = ("issue_cycles_per_score", "valu_mfma_overlap", "tile_sync_cycles",
+              "tile_latency_cycles")
+
+
+def key(c: dict) -> tuple:
+    return (c["BLOCK_N"], c["WAVES"], c["PIPE"])
+
+
+def time_variant(w, variant, iters=10, reps=3) -> float:
+    """Best-of-reps mean time (us) of `iters` back-to-back launches."""
+    import torch
+    from attn_inputs import random_bf16
+    name, B, H, Sq, Skv, d, causal = w
+    if not hasattr(time_variant, "cache") or time_variant.cache[0] != name:
+        q = random_bf16((B, H, Sq, d), 11).cuda()
+        k = random_bf16((B, H, Skv, d), 12).cuda()
+        v = random_bf16((B, H, Skv, d), 13).cuda()
+        o = torch.empty((B, H, Sq, d), dtype=torch.float32, device="cuda")
+        time_variant.cache = (name, q, k, v, o)
+    _, q, k, v, o = time_variant.cache
+    bn, nw, pipe = variant
+    os.environ["ATTN_FORCE_PLAN"] = f"bn={bn},waves={nw},pipe={pipe}"
+    try:
+        for _ in range(3):
+            pa.attn_fwd(q, k, v, o=o, causal=causal)
+        torch.cuda.synchronize()
+        best = float("inf")
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for _ in range(iters):
+                pa.attn_fwd(q, k, v, o=o, causal=causal)
+            b.record()
+            torch.cuda.synchronize()
+            best = min(best, a.elapsed_time(b) / iters * 1e3)
+        return best
+    finally:
+        os.environ.pop("ATTN_FORCE_PLAN", None)
+
+
+def neighbours(pick: tuple, feasible: set) -> list:
+    bns, waves, pipes = (32, 64, 128), (4, 8), (0, 1, 2, 3)
+    bn, nw, pipe = pick
+    out = []
+    for b in bns:
+        for w in waves:
+            for p in pipes:
+                steps = (abs(bns.index(b) - bns.index(bn)) + (w != nw) + abs(p - pipe))
+                if 0 < steps and abs(bns.index(b) - bns.index(bn)) <= 1 and abs(p - pipe) <= 1 \
+                        and (b, w, p) in feasible:
+                    out.append((b, w, p))
+    return out
+
+
+def spearman(a, b) -> float:
+    def ranks(x):
+        order = sorted(range(len(x)), key=lambda i: x[i])
+        r = [0.0] * len(x)
+        for pos, i in enumerate(order):
+            r[i] = pos
+        return r
+    ra, rb = ranks(a), ranks(b)
+    n = len(a)
+    if n < 2:
+        return float("nan")
+    ma, mb = sum(ra) / n, sum(rb) / n
+    num = sum((x - ma) * (y - mb) for x, y in zip(ra, rb))
+    den = math.sqrt(sum((x - ma) ** 2 for x in ra) * sum((y - mb) ** 2 for y in rb))
+    return num / den if den else float("nan")
+
+
+def summarise(w, cands: list, meas: dict) -> dict:
+    rows = [(c["modeled_us"], meas[key(c)], key(c)) for c in cands if key(c) in meas]
+    by_model = sorted(rows)
+    by_meas = sorted(rows, key=lambda r: r[1])
+    pick, best = by_model[0], by_meas[0]
+    feasible = {r[2] for r in rows}
+    nb = neighbours(pick[2], feasible)
+    nb_times = [meas[n] for n in nb]
+    return {
+        "workload": w[0], "candidates": len(rows),
+        "pick": pick[2], "pick_us": pick[1], "pick_modeled_us": pick[0],
+        "best": best[2], "best_us": best[1],
+        "pick_over_best": pick[1] / best[1] - 1.0,
+        "pick_measured_rank": [r[2] for r in by_meas].index(pick[2]) + 1,
+        "best_in_model_top5": best[2] in [r[2] for r in by_model[:5]],
+        "spearman": spearman([r[0] for r in rows], [r[1] for r in rows]),
+        "neighbours": len(nb),
+        "pick_rank_in_neighbourhood": 1 + sum(t < pick[1] for t in nb_times),
+        "rows": [{"variant": r[2], "modeled_us": r[0], "measured_us": r[1]} for r in by_meas],
+    }
+
+
+def fit(data: dict) -> dict:
+    """Least squares on log(modeled / measured) over every measured candidate."""
+    from scipy.optimize import least_squares
+    base = pa.DeviceDesc()
+    pa.lib.attn_query_device(ctypes.byref(base))
+
+    def resid(x):
+        desc = pa.DeviceDesc()
+        ctypes.memmove(ctypes.byref(desc), ctypes.byref(base), ctypes.sizeof(desc))
+        for name, val in zip(CALIBRATED, x):
+            setattr(desc, name, float(val))
+        out = []
+        for w in WORKLOADS:
+            meas = data.get(w[0])
+            if not meas:
+                continue
+            for c in pa.fwd_candidates(*w[1:], desc=desc, device_footprint=True):
+                t = meas.get(key(c))
+                if t:
+                    out.append(math.log(c["modeled_us"]) - math.log(t))
+        return out
+
+    x0 = [getattr(base, n) for n in CALIBRATED]
+    sol = least_squares(resid, x0, bounds=([1.0, 0.0, 0.0, 0.0], [400.0, 0.95, 5000.0, 20000.0]),
+                        diff_step=1e-3)
+    r = resid(sol.x)
+    return {"fields": dict(zip(CALIBRATED, map(float, sol.x))),
+            "rms_log_error": math.sqrt(sum(v * v for v in r) / len(r)), "points": len(r)}
+
+
+def markdown(summaries: list, fitted: dict | None) -> str:
+    out = ["| workload | candidates | planner pick (BN, waves, pipe) | pick vs measured best | "
+           "pick's measured rank | best in model top-5 | Spearman | pick's rank among its "
+           "neighbours |", "|---|---|---|---|---|---|---|---|"]
+    for s in summaries:
+        out.append(f"| {s['workload']} | {s['candidates']} | {s['pick']} {s['pick_us']:.1f} us "
+                   f"(modelled {s['pick_modeled_us']:.1f}) | {s['pick_over_best']:+.1%} "
+                   f"(best {s['best']} {s['best_us']:.1f} us) | {s['pick_measured_rank']} | "
+                   f"{'yes' if s['best_in_model_top5'] else 'no'} | {s['spearman']:.2f} | "
+                   f"{s['pick_rank_in_neighbourhood']} of {s['neighbours'] + 1} |")
+    if fitted:
+        out.append("")
+        out.append(f"Refit of the calibrated fields ({fitted['points']} points, rms log error "
+                   f"{fitted['rms_log_error']:.3f}): " +
+                   ", ".join(f"{k} = {v:.3g}" for k, v in fitted["fields"].items()))
+    return "\n".join(out)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--save", help="write the measurements (JSON)")
+    ap.add_argument("--load", help="reuse measurements (JSON) instead of timing")
+    ap.add_argument("--fit", action="store_true", help="refit the calibrated description fields")
+    ap.add_argument("--markdown", help="write the summary table here")
+    a = ap.parse_args()
+    import torch
+    # torch's HIP runtime must initialise the device before this library's
+    # first HIP call (the plan query below makes one)
+    assert torch.cuda.is_available(), "the ablation needs a HIP device"
+    data = {}
+    if a.load:
+        with open(a.load) as f:
+            raw = json.load(f)
+        data = {w: {tuple(map(int, k.split(","))): t for k, t in m.items()} for w, m in raw.items()}
+    summaries = []
+    for w in WORKLOADS:
+        cands = pa.fwd_candidates(*w[1:])
+        if not a.load:
+            meas = {}
+            for c in cands:
+                meas[key(c)] = time_variant(w, key(c))
+                print(f"{w[0]} {key(c)} modelled {c['modeled_us']:.1f} us measured "
+                      f"{meas[key(c)]:.1f} us", flush=True)
+            data[w[0]] = meas
+        summaries.append(summarise(w, cands, data[w[0]]))
+    if a.save:
+        with open(a.save, "w") as f:
+            json.dump({w: {",".join(map(str, k)): t for k, t in m.items()} for w, m in data.items()},
+                      f, indent=1)
+    fitted = fit(data) if a.fit else None
+    text = markdown(summaries, fitted)
+    print(text)
+    if a.markdown:
+        with open(a.markdown, "w") as f:
+            f.write(text + "\n")
+
+
+if __name__ == "__main__":
+    main()

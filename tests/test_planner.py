@@ -67,8 +67,9 @@ def test_plan_is_deterministic_and_named(w):
     p = pa.parse_plan(a)
     assert p["modeled_us"] > 0 and p["bound"]
     if w[0] == pa.KIND_FWD:
-        assert p["BLOCK_N"] in (32, 64, 128) and p["WAVES"] in (4, 8) and p["PIPE"] in (0, 1, 2)
-        assert p["PIPE"] < 2 or p["WAVES"] == 8
+        assert p["BLOCK_N"] in (32, 64, 128) and p["WAVES"] in (4, 8) and p["PIPE"] in (0, 1, 2, 3)
+        assert p["PIPE"] != 2 or p["WAVES"] == 8
+        assert p["PIPE"] != 3 or p["BLOCK_N"] <= 64
         assert p["BLOCK_M"] == 32 * p["WAVES"]
         assert p["lds_bytes"] <= 160 * 1024
     else:
@@ -136,6 +137,46 @@ def test_decode_split_count_is_bounded_by_keys():
 def test_bad_descriptions_rejected():
     d = spec()
     d.num_cus = 0
+    with pytest.raises(pa.AttnError) as e:
+        plan(d, pa.KIND_FWD, 1, 1, 64, 64, 64)
+    assert e.value.code == pa.ATTN_EINVAL
+
+
+@pytest.mark.parametrize("w", [w for w in WORKLOADS if w[0] == pa.KIND_FWD])
+def test_plan_is_the_argmin_of_the_candidates(w):
+    d = spec()
+    cands = pa.fwd_candidates(*w[1:], desc=d)
+    assert cands, "no feasible candidate"
+    best = min(cands, key=lambda c: c["modeled_us"])
+    p = plan(d, *w)
+    assert p["modeled_us"] == pytest.approx(best["modeled_us"])
+    assert (p["BLOCK_N"], p["WAVES"], p["PIPE"]) in {(c["BLOCK_N"], c["WAVES"], c["PIPE"]) for c in cands}
+
+
+def test_calibrated_fields_shape_the_model():
+    d = spec()
+    base = plan(d, pa.KIND_FWD, 1, 32, 8192, 8192, 128)["modeled_us"]
+    d.issue_cycles_per_score *= 2
+    assert plan(d, pa.KIND_FWD, 1, 32, 8192, 8192, 128)["modeled_us"] > base
+    d = spec()
+    d.valu_mfma_overlap = 0.0
+    assert plan(d, pa.KIND_FWD, 1, 32, 8192, 8192, 128)["modeled_us"] > base
+    d = spec()
+    d.tile_sync_cycles *= 4
+    slow = pa.fwd_candidates(1, 32, 8192, 8192, 128, False, desc=d)
+    fast = pa.fwd_candidates(1, 32, 8192, 8192, 128, False, desc=spec())
+    # synchronisation costs weigh more on narrow tiles (more tiles per row)
+    def ratio(cs, bn):
+        return min(c["modeled_us"] for c in cs if c["BLOCK_N"] == bn)
+    assert ratio(slow, 32) / ratio(fast, 32) > ratio(slow, 128) / ratio(fast, 128)
+
+
+@pytest.mark.parametrize("field,value", [("valu_mfma_overlap", 1.0), ("valu_mfma_overlap", -0.1),
+                                         ("issue_cycles_per_score", -1.0),
+                                         ("tile_sync_cycles", -5.0), ("tile_latency_cycles", -1.0)])
+def test_calibrated_fields_out_of_range_rejected(field, value):
+    d = spec()
+    setattr(d, field, value)
     with pytest.raises(pa.AttnError) as e:
         plan(d, pa.KIND_FWD, 1, 1, 64, 64, 64)
     assert e.value.code == pa.ATTN_EINVAL
