@@ -14,6 +14,8 @@ What each function follows in the paper:
   * ``attn`` / ``attn_probs`` / ``attn_rows`` -- the Flash Attention workload of
     the Evaluation section (matrix multiplication, softmax, value
     aggregation), written as the textbook definition.
+  * ``attn_gqa`` -- the same definition with grouped-query heads and the
+    row log-sum-exp (variants the survey lists as next steps).
   * ``decode_split`` -- the Flash Decode decomposition in the HEG paragraph of
     the latency-modelling section (local softmax per chunk, gather partials,
     global softmax, final output).
@@ -83,9 +85,11 @@ class Oracle:
                                          ci, ci, ci, ci, ci, cf, ci]
         lib.oracle_decode_split.argtypes = [u16p, u16p, u16p, f64p, ci, ci, ci, ci, cf, ci,
                                             f64p, f64p, f64p]
+        lib.oracle_attn_gqa.argtypes = [u16p, u16p, u16p, f64p, f64p, ci, ci, ci, ci, ci, ci,
+                                        cf, ci]
         lib.oracle_num_threads.argtypes = []
         for fn in (lib.oracle_attn, lib.oracle_attn_probs, lib.oracle_attn_rows,
-                   lib.oracle_decode_split, lib.oracle_num_threads):
+                   lib.oracle_decode_split, lib.oracle_num_threads, lib.oracle_attn_gqa):
             fn.restype = ctypes.c_int
         self.lib = lib
         self.path = lib_path
@@ -103,6 +107,21 @@ class Oracle:
                                   B, H, Sq, Skv, d, float(scale), int(bool(causal)))
         _check(rc, "attn")
         return o
+
+    def attn_gqa(self, q, k, v, B, Hq, Hkv, Sq, Skv, d, scale, causal):
+        """(O, lse): grouped-query heads (query head h reads key/value head
+        h // (Hq // Hkv)) and the natural-log log-sum-exp of every row's
+        scores; shapes [B,Hq,Sq,d] and [B,Hq,Sq]."""
+        q, k, v = _bits(q), _bits(k), _bits(v)
+        _sizes(q, k, v, B * Hq * Sq * d, B * Hkv * Skv * d)
+        o = np.empty((B, Hq, Sq, d), dtype=np.float64)
+        lse = np.empty((B, Hq, Sq), dtype=np.float64)
+        rc = self.lib.oracle_attn_gqa(_p(q, ctypes.c_uint16), _p(k, ctypes.c_uint16),
+                                      _p(v, ctypes.c_uint16), _p(o, ctypes.c_double),
+                                      _p(lse, ctypes.c_double), B, Hq, Hkv, Sq, Skv, d,
+                                      float(scale), int(bool(causal)))
+        _check(rc, "attn_gqa")
+        return o, lse
 
     def attn_probs(self, q, k, v, B, H, Sq, Skv, d, scale, causal):
         """(O, P) with P = the softmax weights, shape [B,H,Sq,Skv]."""
@@ -177,6 +196,10 @@ def attn(*a, **kw):
 
 def attn_probs(*a, **kw):
     return default().attn_probs(*a, **kw)
+
+
+def attn_gqa(*a, **kw):
+    return default().attn_gqa(*a, **kw)
 
 
 def attn_rows(*a, **kw):

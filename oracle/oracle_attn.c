@@ -18,6 +18,12 @@
  *   The max is subtracted before exp; that changes rounding only, not the
  *   exact value.
  *
+ *   Variants (not in the paper's evaluation; the survey's next steps):
+ *   grouped-query heads -- query head h of Hq reads key/value head
+ *   h / (Hq / Hkv) of Hkv -- and the log-sum-exp of each row's scores,
+ *       lse_i = log sum_{j in A_i} exp(s_ij)  (natural log),
+ *   so that P_ij = exp(s_ij - lse_i).
+ *
  *   oracle_decode_split follows the paper's decomposition of Flash Decode in
  *   the latency-modelling section (HEG paragraph): a local softmax loop over
  *   each chunk of the sequence axis, then gathering the partial results, a
@@ -68,7 +74,7 @@ static int64_t last_key(int64_t i, int64_t Sq, int64_t Skv, int causal) {
 static void attend_row(const uint16_t* qrow, const uint16_t* kslab,
                        const uint16_t* vslab, int64_t jmax, int64_t Skv,
                        int64_t d, double scale, double* s, double* acc,
-                       double* o_row, double* p_row) {
+                       double* o_row, double* p_row, double* lse) {
     /* matrix multiplication: scores of the allowed keys */
     double m = -INFINITY;
     for (int64_t j = 0; j <= jmax; ++j) {
@@ -91,6 +97,8 @@ static void attend_row(const uint16_t* qrow, const uint16_t* kslab,
         for (int64_t c = 0; c < d; ++c) acc[c] += w * widen_bf16(vslab[j * d + c]);
     }
     for (int64_t c = 0; c < d; ++c) o_row[c] = acc[c] / l;
+    /* log-sum-exp: the stabiliser plus the log of the sum */
+    if (lse) *lse = m + log(l);
     if (p_row) {
         for (int64_t j = 0; j < Skv; ++j) p_row[j] = (j <= jmax) ? s[j] / l : 0.0;
     }
@@ -102,12 +110,20 @@ static int check_dims(int B, int H, int Sq, int Skv, int d, int causal) {
     return 0;
 }
 
+/* Query head h of Hq reads key/value head h / (Hq / Hkv). */
+static int check_heads(int Hq, int Hkv) {
+    if (Hq <= 0 || Hkv <= 0 || Hq % Hkv != 0) return -1;
+    return 0;
+}
+
 static int attend_all(const uint16_t* q, const uint16_t* k, const uint16_t* v,
-                      double* o, double* p, int B, int H, int Sq, int Skv,
-                      int d, float scale, int causal) {
-    int rc = check_dims(B, H, Sq, Skv, d, causal);
+                      double* o, double* p, double* lse, int B, int Hq, int Hkv, int Sq,
+                      int Skv, int d, float scale, int causal) {
+    int rc = check_dims(B, Hq, Sq, Skv, d, causal);
+    if (!rc) rc = check_heads(Hq, Hkv);
     if (rc) return rc;
-    const int64_t rows = (int64_t)B * H * Sq;
+    const int64_t rows = (int64_t)B * Hq * Sq;
+    const int64_t group = Hq / Hkv;
     const double sc = (double)scale;
     int failed = 0;
 #pragma omp parallel
@@ -122,11 +138,14 @@ static int attend_all(const uint16_t* q, const uint16_t* k, const uint16_t* v,
         for (int64_t r = 0; r < rows; ++r) {
             if (!s || !acc) continue;
             const int64_t bh = r / Sq, i = r % Sq;
+            const int64_t b = bh / Hq, h = bh % Hq;
+            const int64_t kvh = b * Hkv + h / group; /* shared key/value head */
             const uint16_t* qrow = q + r * d;
-            const uint16_t* kslab = k + bh * (int64_t)Skv * d;
-            const uint16_t* vslab = v + bh * (int64_t)Skv * d;
+            const uint16_t* kslab = k + kvh * (int64_t)Skv * d;
+            const uint16_t* vslab = v + kvh * (int64_t)Skv * d;
             attend_row(qrow, kslab, vslab, last_key(i, Sq, Skv, causal), Skv, d, sc,
-                       s, acc, o + r * d, p ? p + r * (int64_t)Skv : NULL);
+                       s, acc, o + r * d, p ? p + r * (int64_t)Skv : NULL,
+                       lse ? lse + r : NULL);
         }
         free(s);
         free(acc);
@@ -138,14 +157,25 @@ static int attend_all(const uint16_t* q, const uint16_t* k, const uint16_t* v,
 int oracle_attn(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                 double* o, int B, int H, int Sq, int Skv, int d, float scale,
                 int causal) {
-    return attend_all(q, k, v, o, NULL, B, H, Sq, Skv, d, scale, causal);
+    return attend_all(q, k, v, o, NULL, NULL, B, H, H, Sq, Skv, d, scale, causal);
 }
 
 /* As oracle_attn, and also the probabilities p: fp64 [B][H][Sq][Skv]. */
 int oracle_attn_probs(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                       double* o, double* p, int B, int H, int Sq, int Skv,
                       int d, float scale, int causal) {
-    return attend_all(q, k, v, o, p, B, H, Sq, Skv, d, scale, causal);
+    return attend_all(q, k, v, o, p, NULL, B, H, H, Sq, Skv, d, scale, causal);
+}
+
+/*
+ * Grouped-query heads and the log-sum-exp: q, o [B][Hq][Sq][d]; k, v
+ * [B][Hkv][Skv][d] with Hkv dividing Hq; lse (may be NULL) [B][Hq][Sq].
+ * Returns 0, -1 (bad dims or heads), -2 (causal, Sq > Skv).
+ */
+int oracle_attn_gqa(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                    double* o, double* lse, int B, int Hq, int Hkv, int Sq, int Skv,
+                    int d, float scale, int causal) {
+    return attend_all(q, k, v, o, NULL, lse, B, Hq, Hkv, Sq, Skv, d, scale, causal);
 }
 
 /*
@@ -175,7 +205,8 @@ int oracle_attn_rows(const uint16_t* q, const uint16_t* k, const uint16_t* v,
             if (!s || !acc) continue;
             const int64_t r = rows[n], bh = r / Sq, i = r % Sq;
             attend_row(q + r * d, k + bh * (int64_t)Skv * d, v + bh * (int64_t)Skv * d,
-                       last_key(i, Sq, Skv, causal), Skv, d, sc, s, acc, o + n * d, NULL);
+                       last_key(i, Sq, Skv, causal), Skv, d, sc, s, acc, o + n * d, NULL,
+                       NULL);
         }
         free(s);
         free(acc);

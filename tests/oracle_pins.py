@@ -15,7 +15,11 @@ oracle disagrees with what mathematics or an independent library fixes:
   the tail of a longer query set, outputs are convex combinations of V;
 * the exact value: 50-digit mpmath evaluation on tiny inputs;
 * decode: the split-KV combine equals the unsplit result for every split
-  count, and one key per split gives closed-form partials.
+  count, and one key per split gives closed-form partials;
+* grouped-query heads equal full heads with every key/value head repeated
+  (and PyTorch's attention on them); the row log-sum-exp equals
+  ``torch.logsumexp`` of independently computed scores, exp(s - lse) are the
+  probabilities, and Q = 0 or one key give closed forms.
 
 ``tests/test_oracle.py`` runs every pin on the real oracle and on mutated
 copies of it (each with one planted mistake), and requires every mutant to
@@ -288,6 +292,7 @@ def pin_mpmath_exact(orc):
             _rand((B, H, Skv, d), 2020 + n)
         sc = 0.75
         got = orc.attn(q, k, v, B, H, Sq, Skv, d, sc, causal)
+        got_lse = orc.attn_gqa(q, k, v, B, H, H, Sq, Skv, d, sc, causal)[1]
         qf, kf, vf = (t.double().numpy() for t in (q, k, v))
         for b in range(B):
             for h in range(H):
@@ -297,6 +302,7 @@ def pin_mpmath_exact(orc):
                                                            mpmath.mpf(kf[b, h, j, c])
                                                            for c in range(d)) for j in keys]
                     lse = mpmath.log(mpmath.fsum(mpmath.exp(x) for x in logits))
+                    assert abs(float(lse) - got_lse[b, h, i]) <= 1e-14, "mpmath exact lse"
                     for c in range(d):
                         exact = mpmath.fsum(mpmath.exp(x - lse) * mpmath.mpf(vf[b, h, j, c])
                                             for x, j in zip(logits, keys))
@@ -346,6 +352,80 @@ def pin_rows_subset(orc):
         rows = [0, 5, 17, 35, 20]
         _close(orc.attn_rows(q, k, v, rows, B, H, Sq, Skv, d, 0.5, causal), full[rows],
                atol=0.0, what="row subset")
+
+
+# ------------------------------------------ grouped-query heads and lse
+def _masked_scores(q, k, sc, causal):
+    """fp64 scores scale*q.k (numpy, independent of the oracle), -inf where masked."""
+    s = float(np.float32(sc)) * np.matmul(_f64(q).numpy(), np.swapaxes(_f64(k).numpy(), -1, -2))
+    if causal:
+        Sq, Skv = s.shape[-2], s.shape[-1]
+        i = np.arange(Sq)[:, None]
+        j = np.arange(Skv)[None, :]
+        s = np.where(j <= i + (Skv - Sq), s, -np.inf)
+    return s
+
+
+def pin_gqa_equals_repeated_heads(orc):
+    # Query head h reads key/value head h // g: the same as repeating every
+    # key/value head g times (the library routine sees full heads).
+    B, Hq, Hkv, Sq, Skv, d = 2, 6, 2, 7, 11, 8
+    g = Hq // Hkv
+    q, k, v = _rand((B, Hq, Sq, d), 2500), _rand((B, Hkv, Skv, d), 2501), \
+        _rand((B, Hkv, Skv, d), 2502)
+    kr = k.repeat_interleave(g, dim=1).contiguous()
+    vr = v.repeat_interleave(g, dim=1).contiguous()
+    sc = float(np.float32(0.4))  # the fp32 scale the oracle receives
+    for causal in (False, True):
+        o, _ = orc.attn_gqa(q, k, v, B, Hq, Hkv, Sq, Skv, d, sc, causal)
+        mask = None
+        if causal:
+            i = torch.arange(Sq)[:, None]
+            j = torch.arange(Skv)[None, :]
+            mask = j <= i + (Skv - Sq)
+        _close(o, _sdpa(q, kr, vr, sc, mask=mask), atol=1e-13, what=f"gqa vs sdpa causal={causal}")
+        _close(o, orc.attn(q, kr, vr, B, Hq, Sq, Skv, d, sc, causal), atol=0.0,
+               what="gqa vs repeated-head oracle")
+    # one key/value head for every query head (multi-query)
+    o, _ = orc.attn_gqa(q, k[:, :1].contiguous(), v[:, :1].contiguous(), B, Hq, 1, Sq, Skv, d,
+                        sc, False)
+    _close(o, _sdpa(q, k[:, :1].expand(B, Hq, Skv, d).contiguous(),
+                    v[:, :1].expand(B, Hq, Skv, d).contiguous(), sc), atol=1e-13, what="mqa")
+
+
+def pin_lse_logsumexp(orc):
+    B, Hq, Hkv, Sq, Skv, d = 1, 4, 2, 9, 13, 16
+    q, k, v = _rand((B, Hq, Sq, d), 2600), _rand((B, Hkv, Skv, d), 2601), \
+        _rand((B, Hkv, Skv, d), 2602)
+    kr = k.repeat_interleave(2, dim=1)
+    for causal in (False, True):
+        _, lse = orc.attn_gqa(q, k, v, B, Hq, Hkv, Sq, Skv, d, 0.7, causal)
+        s = torch.from_numpy(_masked_scores(q, kr, 0.7, causal))
+        _close(lse, torch.logsumexp(s, dim=-1).numpy(), atol=1e-13, what=f"lse causal={causal}")
+        # the probabilities are exp(s - lse): they sum to one and match attn_probs
+        p = np.exp(s.numpy() - lse[..., None])
+        _close(p.sum(-1), np.ones_like(lse), atol=1e-13, what="exp(s - lse) sums")
+        _, pref = orc.attn_probs(q, kr.contiguous(), v.repeat_interleave(2, dim=1).contiguous(),
+                                 B, Hq, Sq, Skv, d, 0.7, causal)
+        _close(p, pref, atol=1e-13, what="exp(s - lse) vs probabilities")
+
+
+def pin_lse_closed_forms(orc):
+    # Q = 0: every allowed score is 0, so lse = log(number of allowed keys)
+    B, H, Sq, Skv, d = 1, 2, 5, 8, 8
+    q0 = from_float(torch.zeros(B, H, Sq, d))
+    k, v = _rand((B, H, Skv, d), 2700), _rand((B, H, Skv, d), 2701)
+    _, lse = orc.attn_gqa(q0, k, v, B, H, H, Sq, Skv, d, 0.5, False)
+    _close(lse, np.full((B, H, Sq), math.log(Skv)), atol=1e-15, what="lse Q=0")
+    _, lse = orc.attn_gqa(q0, k, v, B, H, H, Sq, Skv, d, 0.5, True)
+    counts = np.arange(Sq) + (Skv - Sq) + 1
+    _close(lse, np.broadcast_to(np.log(counts), (B, H, Sq)), atol=1e-15, what="lse Q=0 causal")
+    # one key: lse is its score
+    q = _rand((B, H, Sq, d), 2702)
+    _, lse = orc.attn_gqa(q, k[:, :, :1].contiguous(), v[:, :, :1].contiguous(), B, H, H, Sq, 1,
+                          d, 0.5, False)
+    s = float(np.float32(0.5)) * np.einsum("bhic,bhc->bhi", _f64(q).numpy(), _f64(k).numpy()[:, :, 0])
+    _close(lse, s, atol=1e-14, what="lse one key")
 
 
 def pin_rejects_bad_args(orc):

@@ -45,6 +45,10 @@ MUTANTS = [
      "const int64_t j1 = (j0 + chunk < Skv) ? j0 + chunk : Skv - 1;"),
     ("split_skips_boundary_key", "const int64_t j0 = t * chunk;",
      "const int64_t j0 = t * chunk + (t > 0);"),
+    ("gqa_head_mapping", "const int64_t kvh = b * Hkv + h / group;",
+     "const int64_t kvh = b * Hkv + h % Hkv;"),
+    ("lse_without_stabiliser", "if (lse) *lse = m + log(l);", "if (lse) *lse = log(l);"),
+    ("lse_base_two", "if (lse) *lse = m + log(l);", "if (lse) *lse = m + log2(l);"),
 ]
 
 
