@@ -34,6 +34,8 @@
 #ifndef ATTN_H
 #define ATTN_H
 
+#include <stddef.h>
+
 #ifdef __cplusplus
 extern "C" {
 #endif
@@ -46,6 +48,9 @@ extern "C" {
 
 #define ATTN_KIND_FWD 0
 #define ATTN_KIND_DECODE 1
+
+/* attn_fwd_ex flags */
+#define ATTN_OUT_BF16 1        /* o is bf16 (round to nearest even) instead of fp32 */
 
 /*
  * Prefill attention (Flash Attention).
@@ -61,6 +66,24 @@ extern "C" {
  */
 int attn_fwd(const void* q, const void* k, const void* v, float* o, int B, int H, int Sq,
              int Skv, int d, float scale, int causal);
+
+/*
+ * Prefill with grouped-query heads, a bf16 or fp32 output and an optional
+ * log-sum-exp (variants of attn_fwd; attn_fwd(...) is attn_fwd_ex(..., lse =
+ * NULL, Hq = Hkv = H, flags = 0)).
+ *   q: bf16 [B][Hq][Sq][d]   k, v: bf16 [B][Hkv][Skv][d]   Hkv divides Hq;
+ *   query head h reads key/value head h / (Hq / Hkv) (Hkv = 1: multi-query).
+ *   o: [B][Hq][Sq][d], fp32, or bf16 with ATTN_OUT_BF16 (caller-allocated).
+ *   lse: NULL, or fp32 [B][Hq][Sq] (4-byte aligned) receiving each row's
+ *   log-sum-exp of the scaled, masked scores in natural log,
+ *   lse_i = log sum_j exp(scale q_i.k_j), so softmax weights are
+ *   exp(s_ij - lse_i) -- what a caller needs to merge partial attention
+ *   results (split-KV, ring attention).
+ * Errors as attn_fwd; EINVAL also for Hkv not dividing Hq, unknown flags or
+ * a misaligned lse; EUNSUPPORTED if one head's K or V exceeds 2 GiB.
+ */
+int attn_fwd_ex(const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq,
+                int Hkv, int Sq, int Skv, int d, float scale, int causal, int flags);
 
 /*
  * Single-query attention with the KV sequence split across workgroups
@@ -81,6 +104,32 @@ int attn_fwd(const void* q, const void* k, const void* v, float* o, int B, int H
  */
 int attn_decode(const void* q, const void* k, const void* v, float* o, int B, int H, int Skv,
                 int d, int n_splits);
+
+/*
+ * Decode with grouped-query heads, an optional log-sum-exp and an optional
+ * caller-provided workspace (attn_decode(...) is attn_decode_ex(..., lse =
+ * NULL, Hq = Hkv = H, workspace = NULL)).
+ *   q: bf16 [B][Hq][d]   k, v: bf16 [B][Hkv][Skv][d]   o: fp32 [B][Hq][d]
+ *   Hkv divides Hq; query head h reads key/value head h / (Hq / Hkv).  The
+ *   query heads of one key/value head (up to 8 per workgroup) are served
+ *   by the same workgroups, which read each K/V row once for all of them.
+ *   lse: NULL, or fp32 [B][Hq] receiving each row's natural-log
+ *   log-sum-exp (as attn_fwd_ex).
+ *   workspace: NULL (the library's per-stream workspace), or a 16-byte
+ *   aligned device buffer of at least attn_decode_workspace_bytes(...)
+ *   bytes that the caller keeps alive until the stream has passed this
+ *   call; calls that share it must be ordered on one stream.  With a
+ *   caller workspace the call allocates nothing.
+ * Errors as attn_decode; EINVAL also for Hkv not dividing Hq, a misaligned
+ * lse or workspace, or a workspace smaller than needed.
+ */
+int attn_decode_ex(const void* q, const void* k, const void* v, float* o, float* lse, int B,
+                   int Hq, int Hkv, int Skv, int d, int n_splits, void* workspace,
+                   size_t workspace_bytes);
+
+/* Bytes of decode workspace attn_decode_ex needs for this problem (plans
+ * the call; needs the device), or a negative ATTN_E* code. */
+long long attn_decode_workspace_bytes(int B, int Hq, int Hkv, int Skv, int d, int n_splits);
 
 /* Set the HIP stream (hipStream_t, or NULL for the null stream) used by
  * this host thread's subsequent calls.  Returns ATTN_OK. */

@@ -26,9 +26,11 @@ ATTN_EHIP = -3
 ATTN_ENOMEM = -4
 KIND_FWD = 0
 KIND_DECODE = 1
+ATTN_OUT_BF16 = 1
 
 # Entry points declared in include/attn.h.
-EXPORTED = ("attn_fwd", "attn_decode", "attn_set_stream", "attn_get_stream",
+EXPORTED = ("attn_fwd", "attn_decode", "attn_fwd_ex", "attn_decode_ex",
+            "attn_decode_workspace_bytes", "attn_set_stream", "attn_get_stream",
             "attn_last_error", "attn_query_device", "attn_measure_device", "attn_get_plan",
             "attn_get_plan_for")
 
@@ -86,6 +88,11 @@ def _load() -> ctypes.CDLL:
     vp, ci, cf = ctypes.c_void_p, ctypes.c_int, ctypes.c_float
     lib.attn_fwd.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, cf, ci]
     lib.attn_decode.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci]
+    lib.attn_fwd_ex.argtypes = [vp, vp, vp, vp, vp, ci, ci, ci, ci, ci, ci, cf, ci, ci]
+    lib.attn_decode_ex.argtypes = [vp, vp, vp, vp, vp, ci, ci, ci, ci, ci, ci, vp,
+                                   ctypes.c_size_t]
+    lib.attn_decode_workspace_bytes.argtypes = [ci, ci, ci, ci, ci, ci]
+    lib.attn_decode_workspace_bytes.restype = ctypes.c_longlong
     lib.attn_set_stream.argtypes = [vp]
     lib.attn_get_stream.argtypes = []
     lib.attn_get_stream.restype = vp
@@ -98,7 +105,8 @@ def _load() -> ctypes.CDLL:
                                       ci, ctypes.c_char_p, ci]
     lib.attn__fwd_candidates.argtypes = [ctypes.POINTER(DeviceDesc), ci, ci, ci, ci, ci, ci, ci,
                                          ctypes.c_char_p, ci]
-    for fn in (lib.attn_fwd, lib.attn_decode, lib.attn_set_stream, lib.attn_query_device,
+    for fn in (lib.attn_fwd, lib.attn_decode, lib.attn_fwd_ex, lib.attn_decode_ex,
+               lib.attn_set_stream, lib.attn_query_device,
                lib.attn_measure_device, lib.attn_get_plan, lib.attn_get_plan_for,
                lib.attn__fwd_candidates):
         fn.restype = ci
@@ -132,40 +140,73 @@ def _require(t, dtype, shape, name):
         raise ValueError(f"{name} must be contiguous")
 
 
-def attn_fwd(q, k, v, o=None, scale: float | None = None, causal: bool = False):
-    """Prefill attention; returns o fp32 [B,H,Sq,d]."""
+def attn_fwd(q, k, v, o=None, scale: float | None = None, causal: bool = False,
+             out_dtype=None, return_lse: bool = False):
+    """Prefill attention; returns o [B,Hq,Sq,d] (fp32, or out_dtype bf16),
+    and with return_lse also the fp32 row log-sum-exp [B,Hq,Sq].  k and v
+    may have fewer heads than q (grouped-query heads: Hkv divides Hq)."""
     import torch
-    B, H, Sq, d = q.shape
-    Skv = k.shape[2]
-    _require(q, torch.bfloat16, (B, H, Sq, d), "q")
-    _require(k, torch.bfloat16, (B, H, Skv, d), "k")
-    _require(v, torch.bfloat16, (B, H, Skv, d), "v")
+    B, Hq, Sq, d = q.shape
+    Hkv, Skv = k.shape[1], k.shape[2]
+    _require(q, torch.bfloat16, (B, Hq, Sq, d), "q")
+    _require(k, torch.bfloat16, (B, Hkv, Skv, d), "k")
+    _require(v, torch.bfloat16, (B, Hkv, Skv, d), "v")
+    if out_dtype is None:
+        out_dtype = o.dtype if o is not None else torch.float32
+    if out_dtype not in (torch.float32, torch.bfloat16):
+        raise ValueError("out_dtype must be torch.float32 or torch.bfloat16")
     if o is None:
-        o = torch.empty((B, H, Sq, d), dtype=torch.float32, device=q.device)
-    _require(o, torch.float32, (B, H, Sq, d), "o")
+        o = torch.empty((B, Hq, Sq, d), dtype=out_dtype, device=q.device)
+    _require(o, out_dtype, (B, Hq, Sq, d), "o")
+    lse = None
+    if return_lse:
+        lse = torch.empty((B, Hq, Sq), dtype=torch.float32, device=q.device)
     if scale is None:
         scale = 1.0 / math.sqrt(d)
     _set_stream(q)
-    _check(lib.attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), B, H, Sq, Skv, d,
-                        float(scale), int(bool(causal))))
-    return o
+    flags = ATTN_OUT_BF16 if out_dtype == torch.bfloat16 else 0
+    _check(lib.attn_fwd_ex(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                           lse.data_ptr() if lse is not None else None, B, Hq, Hkv, Sq, Skv, d,
+                           float(scale), int(bool(causal)), flags))
+    return (o, lse) if return_lse else o
 
 
-def attn_decode(q, k, v, o=None, n_splits: int = 0):
-    """Split-KV single-query attention; returns o fp32 [B,H,d]."""
+def attn_decode(q, k, v, o=None, n_splits: int = 0, workspace=None, return_lse: bool = False):
+    """Split-KV single-query attention; returns o fp32 [B,Hq,d], and with
+    return_lse also the row log-sum-exp [B,Hq].  k and v may have fewer heads
+    than q (grouped-query heads).  workspace: None (the library's), or a
+    device tensor of at least decode_workspace_bytes(...) bytes."""
     import torch
-    B, H, d = q.shape
-    Skv = k.shape[2]
-    _require(q, torch.bfloat16, (B, H, d), "q")
-    _require(k, torch.bfloat16, (B, H, Skv, d), "k")
-    _require(v, torch.bfloat16, (B, H, Skv, d), "v")
+    B, Hq, d = q.shape
+    Hkv, Skv = k.shape[1], k.shape[2]
+    _require(q, torch.bfloat16, (B, Hq, d), "q")
+    _require(k, torch.bfloat16, (B, Hkv, Skv, d), "k")
+    _require(v, torch.bfloat16, (B, Hkv, Skv, d), "v")
     if o is None:
-        o = torch.empty((B, H, d), dtype=torch.float32, device=q.device)
-    _require(o, torch.float32, (B, H, d), "o")
+        o = torch.empty((B, Hq, d), dtype=torch.float32, device=q.device)
+    _require(o, torch.float32, (B, Hq, d), "o")
+    lse = None
+    if return_lse:
+        lse = torch.empty((B, Hq), dtype=torch.float32, device=q.device)
+    ws_ptr, ws_bytes = None, 0
+    if workspace is not None:
+        if not isinstance(workspace, torch.Tensor) or not workspace.is_cuda or \
+                not workspace.is_contiguous():
+            raise TypeError("workspace must be a contiguous tensor on a HIP device")
+        ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
     _set_stream(q)
-    _check(lib.attn_decode(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), B, H, Skv, d,
-                           int(n_splits)))
-    return o
+    _check(lib.attn_decode_ex(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                              lse.data_ptr() if lse is not None else None, B, Hq, Hkv, Skv, d,
+                              int(n_splits), ws_ptr, ws_bytes))
+    return (o, lse) if return_lse else o
+
+
+def decode_workspace_bytes(B: int, Hq: int, Hkv: int, Skv: int, d: int, n_splits: int = 0) -> int:
+    """Bytes of workspace attn_decode needs with a caller-provided buffer."""
+    n = lib.attn_decode_workspace_bytes(B, Hq, Hkv, Skv, d, int(n_splits))
+    if n < 0:
+        raise AttnError(int(n), last_error())
+    return int(n)
 
 
 def query_device() -> dict:

@@ -17,10 +17,8 @@
 #include "common.h"
 
 namespace attn {
-hipError_t launch_fwd_d64(const FwdPlan&, const void*, const void*, const void*, float*, int,
-                          int, float, uint32_t, int, hipStream_t);
-hipError_t launch_fwd_d128(const FwdPlan&, const void*, const void*, const void*, float*, int,
-                           int, float, uint32_t, int, hipStream_t);
+hipError_t launch_fwd_d64(const FwdPlan&, const FwdArgs&, hipStream_t);
+hipError_t launch_fwd_d128(const FwdPlan&, const FwdArgs&, hipStream_t);
 
 bool fwd_resources_d64(int bn, int waves, int pipe, int causal, KernelRes* r);
 bool fwd_resources_d128(int bn, int waves, int pipe, int causal, KernelRes* r);
@@ -38,22 +36,32 @@ bool fwd_resources_forced(int d, int bn, int waves, int pipe, int causal, Kernel
     return true;
 }
 
-hipError_t launch_fwd(const FwdPlan& p, const void* q, const void* k, const void* v, float* o,
-                      int B, int H, int Sq, int Skv, float scale, int num_xcds,
-                      hipStream_t stream) {
-    (void)B;
-    (void)H;
+hipError_t launch_fwd(const FwdPlan& p, const void* q, const void* k, const void* v, void* o,
+                      float* lse, int group, int out_bf16, int Sq, int Skv, float scale,
+                      int num_xcds, hipStream_t stream) {
     // softmax in base 2: exp(x) = 2^(x*log2 e); a negative scale is applied
     // as an exact sign flip of Q.  The kernel needs a factor > 0 (masked
     // scores are -inf); a zero scale becomes the smallest normal float, with
     // which every exponent rounds to 0 and the weights are exactly equal.
     double s = fabs((double)scale) * 1.4426950408889634;
     if (s < (double)FLT_MIN) s = (double)FLT_MIN;
-    const uint32_t q_sign = scale < 0.f ? 0x80008000u : 0u;
-    if (p.d == 64)
-        return launch_fwd_d64(p, q, k, v, o, Sq, Skv, (float)s, q_sign, num_xcds, stream);
-    if (p.d == 128)
-        return launch_fwd_d128(p, q, k, v, o, Sq, Skv, (float)s, q_sign, num_xcds, stream);
+    FwdArgs a;
+    a.q = static_cast<const uint16_t*>(q);
+    a.k = static_cast<const uint16_t*>(k);
+    a.v = static_cast<const uint16_t*>(v);
+    a.o = o;
+    a.lse = lse;
+    a.Sq = Sq;
+    a.Skv = Skv;
+    a.n_qtiles = p.n_qtiles;
+    a.n_wg = (int)p.grid;
+    a.num_xcds = num_xcds;
+    a.group = group;
+    a.out_bf16 = out_bf16;
+    a.scale_log2 = (float)s;
+    a.q_sign = scale < 0.f ? 0x80008000u : 0u;
+    if (p.d == 64) return launch_fwd_d64(p, a, stream);
+    if (p.d == 128) return launch_fwd_d128(p, a, stream);
     return hipErrorInvalidValue;
 }
 }  // namespace attn
@@ -100,7 +108,7 @@ struct DeviceState {
 std::mutex g_mu;
 std::map<int, DeviceState> g_devices;
 std::map<std::tuple<int, int, int, int, int, int, int, int>, FwdPlan> g_fwd_cache;
-std::map<std::tuple<int, int, int, int, int, int>, DecodePlan> g_dec_cache;
+std::map<std::tuple<int, int, int, int, int, int, int>, DecodePlan> g_dec_cache;
 
 // Structural properties from the runtime; performance properties from the
 // built-in gfx950 description.
@@ -227,7 +235,7 @@ int attn_get_plan_for(const attn_device_desc* desc, int kind, int B, int H, int 
     }
     if (kind == ATTN_KIND_DECODE) {
         DecodePlan p;
-        if (!plan_decode(*desc, B, H, Skv, d, n_splits, &p))
+        if (!plan_decode(*desc, B, H, H, Skv, d, n_splits, &p))
             return fail(ATTN_EUNSUPPORTED, "no feasible decode plan");
         return format_decode_plan(p, buf, buflen);
     }
@@ -272,14 +280,21 @@ int attn_get_plan(int kind, int B, int H, int Sq, int Skv, int d, int causal, in
     return attn_get_plan_for(nullptr, kind, B, H, Sq, Skv, d, causal, n_splits, buf, buflen);
 }
 
-int attn_fwd(const void* q, const void* k, const void* v, float* o, int B, int H, int Sq,
-             int Skv, int d, float scale, int causal) {
-    int rc = validate_common(q, k, v, o, B, H, Skv, d);
+int attn_fwd_ex(const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq,
+                int Hkv, int Sq, int Skv, int d, float scale, int causal, int flags) {
+    int rc = validate_common(q, k, v, o, B, Hq, Skv, d);
     if (rc) return rc;
     if (Sq <= 0) return fail(ATTN_EINVAL, "Sq must be positive (got %d)", Sq);
+    if (Hkv <= 0 || Hq % Hkv != 0)
+        return fail(ATTN_EINVAL, "Hkv (%d) must be positive and divide Hq (%d)", Hkv, Hq);
+    if (flags & ~ATTN_OUT_BF16) return fail(ATTN_EINVAL, "unknown flags 0x%x", flags);
+    if (lse && ((uintptr_t)lse & 3u)) return fail(ATTN_EINVAL, "lse must be 4-byte aligned");
     if (!isfinite(scale)) return fail(ATTN_EINVAL, "scale must be finite");
     if (causal && Sq > Skv)
         return fail(ATTN_EUNSUPPORTED, "causal attention needs Sq <= Skv (Sq=%d Skv=%d)", Sq, Skv);
+    if ((long long)Skv * d * 2 > 0x7fffffffLL)
+        return fail(ATTN_EUNSUPPORTED, "one head's K or V (%lld bytes) exceeds 2 GiB",
+                    (long long)Skv * d * 2);
     DeviceState* st = nullptr;
     rc = device_state(&st);
     if (rc) return rc;
@@ -288,49 +303,91 @@ int attn_fwd(const void* q, const void* k, const void* v, float* o, int B, int H
     FwdPlan plan;
     int fbn, fw, fpipe;
     if (forced_fwd(&fbn, &fw, &fpipe)) {
-        if (!plan_fwd_fixed(st->desc, B, H, Sq, Skv, d, c, fbn, fw, fpipe, &plan,
+        if (!plan_fwd_fixed(st->desc, B, Hq, Sq, Skv, d, c, fbn, fw, fpipe, &plan,
                             fwd_resources_forced))
             return fail(ATTN_EINVAL, "ATTN_FORCE_PLAN names an infeasible or unknown tile");
     } else {
         std::lock_guard<std::mutex> lk(g_mu);
-        auto key = std::make_tuple(B, H, Sq, Skv, d, c, st->desc.num_cus, 0);
+        auto key = std::make_tuple(B, Hq, Sq, Skv, d, c, st->desc.num_cus, 0);
         auto it = g_fwd_cache.find(key);
         if (it != g_fwd_cache.end()) {
             plan = it->second;
         } else {
-            if (!plan_fwd(st->desc, B, H, Sq, Skv, d, c, &plan, fwd_resources))
+            if (!plan_fwd(st->desc, B, Hq, Sq, Skv, d, c, &plan, fwd_resources))
                 return fail(ATTN_EUNSUPPORTED, "no feasible prefill plan for this shape");
             g_fwd_cache[key] = plan;
         }
     }
-    hipError_t e = launch_fwd(plan, q, k, v, o, B, H, Sq, Skv, scale, st->desc.num_xcds, t_stream);
+    hipError_t e = launch_fwd(plan, q, k, v, o, lse, Hq / Hkv, (flags & ATTN_OUT_BF16) ? 1 : 0,
+                              Sq, Skv, scale, st->desc.num_xcds, t_stream);
     if (e != hipSuccess) return fail_hip(e, "prefill launch");
     return ATTN_OK;
 }
 
-int attn_decode(const void* q, const void* k, const void* v, float* o, int B, int H, int Skv,
-                int d, int n_splits) {
-    int rc = validate_common(q, k, v, o, B, H, Skv, d);
+int attn_fwd(const void* q, const void* k, const void* v, float* o, int B, int H, int Sq,
+             int Skv, int d, float scale, int causal) {
+    return attn_fwd_ex(q, k, v, o, nullptr, B, H, H, Sq, Skv, d, scale, causal, 0);
+}
+
+// Plan of one decode call (cached per shape).
+static int decode_plan(DeviceState* st, int B, int Hq, int Hkv, int Skv, int d, int n_splits,
+                       DecodePlan* plan) {
+    std::lock_guard<std::mutex> lk(g_mu);
+    auto key = std::make_tuple(B, Hq, Hkv, Skv, d, n_splits, st->desc.num_cus);
+    auto it = g_dec_cache.find(key);
+    if (it != g_dec_cache.end()) {
+        *plan = it->second;
+        return ATTN_OK;
+    }
+    if (!plan_decode(st->desc, B, Hq, Hkv, Skv, d, n_splits, plan))
+        return fail(ATTN_EUNSUPPORTED, "no feasible decode plan for this shape");
+    g_dec_cache[key] = *plan;
+    return ATTN_OK;
+}
+
+static int validate_decode(const void* q, const void* k, const void* v, const void* o, int B,
+                           int Hq, int Hkv, int Skv, int d) {
+    int rc = validate_common(q, k, v, o, B, Hq, Skv, d);
     if (rc) return rc;
+    if (Hkv <= 0 || Hq % Hkv != 0)
+        return fail(ATTN_EINVAL, "Hkv (%d) must be positive and divide Hq (%d)", Hkv, Hq);
+    return ATTN_OK;
+}
+
+long long attn_decode_workspace_bytes(int B, int Hq, int Hkv, int Skv, int d, int n_splits) {
+    if (B <= 0 || Hq <= 0 || Hkv <= 0 || Hq % Hkv != 0 || Skv <= 0)
+        return fail(ATTN_EINVAL, "bad dimensions");
+    if (d != 64 && d != 128) return fail(ATTN_EUNSUPPORTED, "head dim %d not in {64, 128}", d);
+    DeviceState* st = nullptr;
+    int rc = device_state(&st);
+    if (rc) return rc;
+    DecodePlan plan;
+    rc = decode_plan(st, B, Hq, Hkv, Skv, d, n_splits, &plan);
+    if (rc) return rc;
+    return (long long)B * Hq * plan.n_splits * (d + 2) * (long long)sizeof(float);
+}
+
+int attn_decode_ex(const void* q, const void* k, const void* v, float* o, float* lse, int B,
+                   int Hq, int Hkv, int Skv, int d, int n_splits, void* workspace,
+                   size_t workspace_bytes) {
+    int rc = validate_decode(q, k, v, o, B, Hq, Hkv, Skv, d);
+    if (rc) return rc;
+    if (lse && ((uintptr_t)lse & 3u)) return fail(ATTN_EINVAL, "lse must be 4-byte aligned");
+    if (workspace && !aligned16(workspace))
+        return fail(ATTN_EINVAL, "workspace must be 16-byte aligned");
     DeviceState* st = nullptr;
     rc = device_state(&st);
     if (rc) return rc;
     DecodePlan plan;
-    {
-        std::lock_guard<std::mutex> lk(g_mu);
-        auto key = std::make_tuple(B, H, Skv, d, n_splits, st->desc.num_cus);
-        auto it = g_dec_cache.find(key);
-        if (it != g_dec_cache.end()) {
-            plan = it->second;
-        } else {
-            if (!plan_decode(st->desc, B, H, Skv, d, n_splits, &plan))
-                return fail(ATTN_EUNSUPPORTED, "no feasible decode plan for this shape");
-            g_dec_cache[key] = plan;
-        }
-    }
-    const size_t ws_bytes = (size_t)B * H * plan.n_splits * (d + 2) * sizeof(float);
-    void* ws = nullptr;
-    {
+    rc = decode_plan(st, B, Hq, Hkv, Skv, d, n_splits, &plan);
+    if (rc) return rc;
+    const size_t ws_bytes = (size_t)B * Hq * plan.n_splits * (d + 2) * sizeof(float);
+    void* ws = workspace;
+    if (ws) {
+        if (workspace_bytes < ws_bytes)
+            return fail(ATTN_EINVAL, "workspace of %zu bytes, %zu needed", workspace_bytes,
+                        ws_bytes);
+    } else {
         std::lock_guard<std::mutex> lk(g_mu);
         Workspace& w = st->ws[t_stream];
         if (w.bytes < ws_bytes) {
@@ -356,10 +413,15 @@ int attn_decode(const void* q, const void* k, const void* v, float* o, int B, in
         ws = w.ptr;
     }
     const float scale = (float)(1.0 / sqrt((double)d));
-    const hipError_t e =
-        launch_decode(plan, q, k, v, o, static_cast<float*>(ws), B, H, Skv, scale, t_stream);
+    const hipError_t e = launch_decode(plan, q, k, v, o, lse, static_cast<float*>(ws), B, Hq,
+                                       Hkv, Skv, scale, t_stream);
     if (e != hipSuccess) return fail_hip(e, "decode launch");
     return ATTN_OK;
+}
+
+int attn_decode(const void* q, const void* k, const void* v, float* o, int B, int H, int Skv,
+                int d, int n_splits) {
+    return attn_decode_ex(q, k, v, o, nullptr, B, H, H, Skv, d, n_splits, nullptr, 0);
 }
 
 }  // extern "C"

@@ -34,6 +34,7 @@ struct DecodePlan {
     int chunk = 0;     // keys per split
     int threads = 0;   // threads per partial workgroup
     int unroll = 0;    // keys per lane group per loop step
+    int heads_per_wg = 1;  // query heads of one key/value group served together
     int wg_per_cu = 0;
     long long grid = 0;
     double modeled_us = 0.0;
@@ -52,6 +53,23 @@ constexpr int kDecodeUnroll = 8;
 constexpr int fwd_lds_bytes(int d, int bn, int pipe) {
     return (pipe == 0 ? 1 : 2) * (bn * (d + 8) + bn * (d + 32)) * 2;
 }
+
+// Arguments of one prefill launch (every variant takes the same struct).
+struct FwdArgs {
+    const uint16_t* q;  // bf16 [B][Hq][Sq][D]
+    const uint16_t* k;  // bf16 [B][Hkv][Skv][D]
+    const uint16_t* v;
+    void* o;            // [B][Hq][Sq][D], fp32 or bf16 (out_bf16)
+    float* lse;         // [B][Hq][Sq] natural-log log-sum-exp, or null
+    int Sq, Skv;
+    int n_qtiles;       // q-tiles per head
+    int n_wg;           // grid size
+    int num_xcds;
+    int group;          // query heads per key/value head
+    int out_bf16;
+    float scale_log2;   // |scale| * log2(e), > 0
+    uint32_t q_sign;    // sign bits xor-ed into Q (negative scale)
+};
 
 // Resource usage of one compiled prefill variant, as the runtime reports it:
 // resident workgroups per CU (registers and LDS together) and private
@@ -76,19 +94,21 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
 int plan_fwd_all(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d, int causal,
                  FwdPlan* out, int cap, FwdResFn res = nullptr);
 bool fwd_resources(int d, int bn, int waves, int pipe, int causal, KernelRes* out);
-bool plan_decode(const attn_device_desc& desc, int B, int H, int Skv, int d, int n_splits,
-                 DecodePlan* out);
+bool plan_decode(const attn_device_desc& desc, int B, int Hq, int Hkv, int Skv, int d,
+                 int n_splits, DecodePlan* out);
 int format_fwd_plan(const FwdPlan& p, char* buf, int buflen);
 int format_decode_plan(const DecodePlan& p, char* buf, int buflen);
 
 hipError_t measure_device(attn_device_desc* d);
 
 // Launchers (defined next to the kernels).
-hipError_t launch_fwd(const FwdPlan& p, const void* q, const void* k, const void* v, float* o,
-                      int B, int H, int Sq, int Skv, float scale, int num_xcds,
-                      hipStream_t stream);
+hipError_t launch_fwd(const FwdPlan& p, const void* q, const void* k, const void* v, void* o,
+                      float* lse, int group, int out_bf16, int Sq, int Skv, float scale,
+                      int num_xcds, hipStream_t stream);
 hipError_t launch_decode(const DecodePlan& p, const void* q, const void* k, const void* v,
-                         float* o, float* workspace, int B, int H, int Skv, float scale,
-                         hipStream_t stream);
+                         float* o, float* lse, float* workspace, int B, int Hq, int Hkv, int Skv,
+                         float scale, hipStream_t stream);
+// Query heads of one key/value group that a decode workgroup serves together.
+int decode_heads_per_wg(int group);
 
 }  // namespace attn

@@ -36,38 +36,50 @@ __device__ __forceinline__ float group_sum(float x) {
     return x;
 }
 
-template <int D, int NT, int U>
+// GQ query heads that share one key/value head (grouped-query attention) run
+// in the same workgroup, so each K and V row is read from memory once for
+// all of them: a lane keeps GQ query slices, GQ online-softmax states and GQ
+// output slices, and every loaded key is scored against each query.
+template <int D, int NT, int U, int GQ>
 __global__ __launch_bounds__(NT) void decode_partial_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, float* __restrict__ ws_m, float* __restrict__ ws_l,
-    float* __restrict__ ws_o, int Skv, int chunk, int n_splits, float scale_log2) {
+    float* __restrict__ ws_o, int Skv, int chunk, int n_splits, int group, float scale_log2) {
     constexpr int G = D / 8;      // lanes per key
     constexpr int NG = NT / G;    // lane groups (keys per step) in the workgroup
     const int tid = threadIdx.x;
     const int gid = tid / G, sub = tid % G;
     const int split = blockIdx.x % n_splits;
-    const long long bh = blockIdx.x / n_splits;
+    // blockIdx / n_splits enumerates (b, query-head block of GQ heads)
+    const long long hb = blockIdx.x / n_splits;
+    const long long bh0 = hb * GQ;          // first query head (flat b*Hq + h)
+    const long long kvh = bh0 / group;      // the key/value head they share
     const int j0 = split * chunk;
     const int j1 = min(Skv, j0 + chunk);
 
-    // this lane's 8 query dims, pre-multiplied by scale*log2(e)
-    float qv[8];
-    {
-        const u32x4 w = *reinterpret_cast<const u32x4*>(Q + bh * D + sub * 8);
+    // this lane's 8 dims of each query, pre-multiplied by scale*log2(e)
+    float qv[GQ][8];
+#pragma unroll
+    for (int g = 0; g < GQ; ++g) {
+        const u32x4 w = *reinterpret_cast<const u32x4*>(Q + (bh0 + g) * D + sub * 8);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            qv[2 * e] = __uint_as_float(w[e] << 16) * scale_log2;
-            qv[2 * e + 1] = __uint_as_float(w[e] & 0xffff0000u) * scale_log2;
+            qv[g][2 * e] = __uint_as_float(w[e] << 16) * scale_log2;
+            qv[g][2 * e + 1] = __uint_as_float(w[e] & 0xffff0000u) * scale_log2;
         }
     }
 
-    const uint16_t* Kb = K + bh * (long long)Skv * D + sub * 8;
-    const uint16_t* Vb = V + bh * (long long)Skv * D + sub * 8;
+    const uint16_t* Kb = K + kvh * (long long)Skv * D + sub * 8;
+    const uint16_t* Vb = V + kvh * (long long)Skv * D + sub * 8;
 
-    float m = -INFINITY, l = 0.f;
-    float o[8];
+    float m[GQ], l[GQ], o[GQ][8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) o[e] = 0.f;
+    for (int g = 0; g < GQ; ++g) {
+        m[g] = -INFINITY;
+        l[g] = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[g][e] = 0.f;
+    }
 
     for (int base = j0; base < j1; base += U * NG) {
         u32x4 kr[U], vr[U];
@@ -78,74 +90,85 @@ __global__ __launch_bounds__(NT) void decode_partial_kernel(
             kr[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(Kb + (long long)key * D));
             vr[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(Vb + (long long)key * D));
         }
-        float s[U];
-        float mx = -INFINITY;
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            float acc = 0.f;
+        for (int g = 0; g < GQ; ++g) {
+            float s[U];
+            float mx = -INFINITY;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                acc = fmaf(qv[2 * e], __uint_as_float(kr[u][e] << 16), acc);
-                acc = fmaf(qv[2 * e + 1], __uint_as_float(kr[u][e] & 0xffff0000u), acc);
+            for (int u = 0; u < U; ++u) {
+                float acc = 0.f;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    acc = fmaf(qv[g][2 * e], __uint_as_float(kr[u][e] << 16), acc);
+                    acc = fmaf(qv[g][2 * e + 1], __uint_as_float(kr[u][e] & 0xffff0000u), acc);
+                }
+                acc = group_sum<G>(acc);
+                s[u] = (base + u * NG + gid < j1) ? acc : -INFINITY;
+                mx = fmaxf(mx, s[u]);
             }
-            acc = group_sum<G>(acc);
-            s[u] = (base + u * NG + gid < j1) ? acc : -INFINITY;
-            mx = fmaxf(mx, s[u]);
-        }
-        const float m_new = fmaxf(m, mx);
-        const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-        const float alpha = __builtin_amdgcn_exp2f(m - m_use);
-        l *= alpha;
+            const float m_new = fmaxf(m[g], mx);
+            const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+            const float alpha = __builtin_amdgcn_exp2f(m[g] - m_use);
+            l[g] *= alpha;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) o[e] *= alpha;
+            for (int e = 0; e < 8; ++e) o[g][e] *= alpha;
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const float p = __builtin_amdgcn_exp2f(s[u] - m_use);
-            l += p;
+            for (int u = 0; u < U; ++u) {
+                const float p = __builtin_amdgcn_exp2f(s[u] - m_use);
+                l[g] += p;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                o[2 * e] = fmaf(p, __uint_as_float(vr[u][e] << 16), o[2 * e]);
-                o[2 * e + 1] = fmaf(p, __uint_as_float(vr[u][e] & 0xffff0000u), o[2 * e + 1]);
+                for (int e = 0; e < 4; ++e) {
+                    o[g][2 * e] = fmaf(p, __uint_as_float(vr[u][e] << 16), o[g][2 * e]);
+                    o[g][2 * e + 1] =
+                        fmaf(p, __uint_as_float(vr[u][e] & 0xffff0000u), o[g][2 * e + 1]);
+                }
             }
+            m[g] = m_new;
         }
-        m = m_new;
     }
 
-    // merge the NG lane groups of this workgroup
+    // merge the NG lane groups of this workgroup, one query at a time
     __shared__ float sm[NG], sl[NG];
     __shared__ float so[NG][D + 4];
-    if (sub == 0) {
-        sm[gid] = m;
-        sl[gid] = l;
-    }
 #pragma unroll
-    for (int e = 0; e < 8; ++e) so[gid][sub * 8 + e] = o[e];
-    __syncthreads();
-    const long long out = bh * n_splits + split;
-    for (int c = tid; c < D; c += NT) {
-        float M = -INFINITY;
-        for (int g = 0; g < NG; ++g) M = fmaxf(M, sm[g]);
-        float L = 0.f, acc = 0.f;
-        for (int g = 0; g < NG; ++g) {
-            const float w = __builtin_amdgcn_exp2f(sm[g] - M);
-            L = fmaf(w, sl[g], L);
-            acc = fmaf(w, so[g][c], acc);
+    for (int g = 0; g < GQ; ++g) {
+        if (sub == 0) {
+            sm[gid] = m[g];
+            sl[gid] = l[g];
         }
-        ws_o[out * D + c] = acc;
-        if (c == 0) {
-            ws_m[out] = M;
-            ws_l[out] = L;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) so[gid][sub * 8 + e] = o[g][e];
+        __syncthreads();
+        const long long out = (bh0 + g) * n_splits + split;
+        for (int c = tid; c < D; c += NT) {
+            float M = -INFINITY;
+            for (int q = 0; q < NG; ++q) M = fmaxf(M, sm[q]);
+            float L = 0.f, acc = 0.f;
+            for (int q = 0; q < NG; ++q) {
+                const float w = __builtin_amdgcn_exp2f(sm[q] - M);
+                L = fmaf(w, sl[q], L);
+                acc = fmaf(w, so[q][c], acc);
+            }
+            ws_o[out * D + c] = acc;
+            if (c == 0) {
+                ws_m[out] = M;
+                ws_l[out] = L;
+            }
         }
+        __syncthreads();  // the LDS merge buffers are reused by the next query
     }
 }
 
 // Global softmax over the split partials and the final output:
-//   M = max_s m_s, w_s = 2^(m_s - M), o = sum_s w_s o_s / sum_s w_s l_s.
+//   M = max_s m_s, w_s = 2^(m_s - M), o = sum_s w_s o_s / sum_s w_s l_s,
+// and optionally the log-sum-exp of the row's scores (natural log),
+//   lse = (M + log2(sum_s w_s l_s)) * ln 2.
 template <int D>
 __global__ __launch_bounds__(D) void decode_combine_kernel(const float* __restrict__ ws_m,
                                                            const float* __restrict__ ws_l,
                                                            const float* __restrict__ ws_o,
-                                                           float* __restrict__ O, int n_splits) {
+                                                           float* __restrict__ O,
+                                                           float* __restrict__ lse, int n_splits) {
     const long long bh = blockIdx.x;
     const int c = threadIdx.x;
     const float* mm = ws_m + bh * n_splits;
@@ -160,34 +183,54 @@ __global__ __launch_bounds__(D) void decode_combine_kernel(const float* __restri
         acc = fmaf(w, oo[(long long)s * D], acc);
     }
     O[bh * D + c] = acc / L;
+    if (lse && c == 0) lse[bh] = (M + __builtin_log2f(L)) * 0.69314718055994531f;
+}
+
+template <int D, int GQ>
+static hipError_t launch_partial(const DecodePlan& p, const void* q, const void* k,
+                                 const void* v, float* ws_m, float* ws_l, float* ws_o,
+                                 long long BHq, int Skv, int group, float scale_log2,
+                                 hipStream_t st) {
+    // fewer keys in flight per lane group when each key serves many queries
+    constexpr int U = GQ >= 4 ? 4 : kDecodeUnroll;
+    hipLaunchKernelGGL((decode_partial_kernel<D, kDecodeThreads, U, GQ>),
+                       dim3((unsigned)(BHq / GQ * p.n_splits)), dim3(kDecodeThreads), 0, st,
+                       static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                       static_cast<const uint16_t*>(v), ws_m, ws_l, ws_o, Skv, p.chunk,
+                       p.n_splits, group, scale_log2);
+    return hipGetLastError();
 }
 
 template <int D>
 static hipError_t launch_decode_d(const DecodePlan& p, const void* q, const void* k,
-                                  const void* v, float* o, float* ws, int B, int H, int Skv,
-                                  float scale_log2, hipStream_t st) {
-    const long long BH = (long long)B * H;
+                                  const void* v, float* o, float* lse, float* ws, int B, int Hq,
+                                  int Hkv, int Skv, float scale_log2, hipStream_t st) {
+    const long long BHq = (long long)B * Hq;
+    const int group = Hq / Hkv;
     float* ws_m = ws;
-    float* ws_l = ws + BH * p.n_splits;
-    float* ws_o = ws + 2 * BH * p.n_splits;
-    hipLaunchKernelGGL((decode_partial_kernel<D, kDecodeThreads, kDecodeUnroll>),
-                       dim3((unsigned)(BH * p.n_splits)), dim3(kDecodeThreads), 0, st,
-                       static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
-                       static_cast<const uint16_t*>(v), ws_m, ws_l, ws_o, Skv, p.chunk,
-                       p.n_splits, scale_log2);
-    hipError_t e = hipGetLastError();
+    float* ws_l = ws + BHq * p.n_splits;
+    float* ws_o = ws + 2 * BHq * p.n_splits;
+    hipError_t e = hipErrorInvalidValue;
+    switch (decode_heads_per_wg(group)) {
+        case 8: e = launch_partial<D, 8>(p, q, k, v, ws_m, ws_l, ws_o, BHq, Skv, group, scale_log2, st); break;
+        case 4: e = launch_partial<D, 4>(p, q, k, v, ws_m, ws_l, ws_o, BHq, Skv, group, scale_log2, st); break;
+        case 2: e = launch_partial<D, 2>(p, q, k, v, ws_m, ws_l, ws_o, BHq, Skv, group, scale_log2, st); break;
+        default: e = launch_partial<D, 1>(p, q, k, v, ws_m, ws_l, ws_o, BHq, Skv, group, scale_log2, st);
+    }
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((decode_combine_kernel<D>), dim3((unsigned)BH), dim3(D), 0, st, ws_m, ws_l,
-                       ws_o, o, p.n_splits);
+    hipLaunchKernelGGL((decode_combine_kernel<D>), dim3((unsigned)BHq), dim3(D), 0, st, ws_m, ws_l,
+                       ws_o, o, lse, p.n_splits);
     return hipGetLastError();
 }
 
 hipError_t launch_decode(const DecodePlan& p, const void* q, const void* k, const void* v,
-                         float* o, float* workspace, int B, int H, int Skv, float scale,
-                         hipStream_t stream) {
+                         float* o, float* lse, float* workspace, int B, int Hq, int Hkv, int Skv,
+                         float scale, hipStream_t stream) {
     const float scale_log2 = (float)((double)scale * 1.4426950408889634);
-    if (p.d == 64) return launch_decode_d<64>(p, q, k, v, o, workspace, B, H, Skv, scale_log2, stream);
-    if (p.d == 128) return launch_decode_d<128>(p, q, k, v, o, workspace, B, H, Skv, scale_log2, stream);
+    if (p.d == 64)
+        return launch_decode_d<64>(p, q, k, v, o, lse, workspace, B, Hq, Hkv, Skv, scale_log2, stream);
+    if (p.d == 128)
+        return launch_decode_d<128>(p, q, k, v, o, lse, workspace, B, Hq, Hkv, Skv, scale_log2, stream);
     return hipErrorInvalidValue;
 }
 

@@ -26,20 +26,13 @@ static bool with_variant(int bn, int waves, int pipe, int causal, F& f) {
 namespace {
 struct Launch {
     const FwdPlan& p;
-    const void *q, *k, *v;
-    float* o;
-    int Sq, Skv;
-    float scale_log2;
-    uint32_t q_sign;
-    int num_xcds;
+    const FwdArgs& a;
     hipStream_t st;
     hipError_t err = hipErrorInvalidValue;
     template <int BN, int NW, int PIPE, bool CAUSAL>
     void run() {
         hipLaunchKernelGGL((fwd_kernel<64, BN, NW, PIPE, CAUSAL>), dim3((unsigned)p.grid),
-                           dim3(NW * 64), 0, st, static_cast<const uint16_t*>(q),
-                           static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), o,
-                           Sq, Skv, p.n_qtiles, (int)p.grid, num_xcds, scale_log2, q_sign);
+                           dim3(NW * 64), 0, st, a);
         err = hipGetLastError();
     }
 };
@@ -63,10 +56,8 @@ struct Resources {
 };
 }  // namespace
 
-hipError_t launch_fwd_d64(const FwdPlan& p, const void* q, const void* k, const void* v,
-                            float* o, int Sq, int Skv, float scale_log2, uint32_t q_sign,
-                            int num_xcds, hipStream_t st) {
-    Launch l{p, q, k, v, o, Sq, Skv, scale_log2, q_sign, num_xcds, st};
+hipError_t launch_fwd_d64(const FwdPlan& p, const FwdArgs& a, hipStream_t st) {
+    Launch l{p, a, st};
     if (!with_variant(p.block_n, p.waves, p.pipe, p.causal, l)) return hipErrorInvalidValue;
     return l.err;
 }

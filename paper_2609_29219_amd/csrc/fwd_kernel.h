@@ -65,6 +65,8 @@
 
 #include <type_traits>
 
+#include "common.h"
+
 namespace attn {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -76,6 +78,7 @@ typedef short s16x8 __attribute__((ext_vector_type(8)));
 
 // Slack (log2 units) before the running max of a row is moved.
 static constexpr float kRescaleSlack = 8.0f;
+static constexpr float kLn2 = 0.69314718055994531f;
 
 template <int D, int BN>
 struct FwdLds {
@@ -130,9 +133,14 @@ constexpr int fwd_waves_per_eu() {
 
 template <int D, int BN, int NW, int PIPE, bool CAUSAL>
 __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) void fwd_kernel(
-    const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
-    const uint16_t* __restrict__ V, float* __restrict__ O, int Sq, int Skv, int n_qtiles,
-    int n_wg, int num_xcds, float scale_log2, uint32_t q_sign) {
+    const FwdArgs args) {
+    const uint16_t* __restrict__ Q = args.q;
+    const uint16_t* __restrict__ K = args.k;
+    const uint16_t* __restrict__ V = args.v;
+    const int Sq = args.Sq, Skv = args.Skv, n_qtiles = args.n_qtiles, n_wg = args.n_wg;
+    const int num_xcds = args.num_xcds;
+    const float scale_log2 = args.scale_log2;
+    const uint32_t q_sign = args.q_sign;
     static_assert(PIPE != 2 || NW == 8, "the ping-pong schedule pairs 4 waves with 4 waves");
     static_assert(PIPE != 3 || BN <= 64, "two score tiles in registers");
     constexpr int BM = NW * 32;
@@ -173,7 +181,8 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     const int unit = logical % units;
     const int n_pass = (CAUSAL && n_qtiles - 1 - unit != unit) ? 2 : 1;
     const int diag = Skv - Sq;  // causal: key j allowed iff j <= row + diag
-    const long long kv_base = (long long)bh * Skv * D;
+    // grouped-query heads: query head bh reads key/value head bh / group
+    const long long kv_base = (long long)(bh / args.group) * Skv * D;
     const uint16_t* Kb = K + kv_base;
     const uint16_t* Vb = V + kv_base;
 
@@ -702,17 +711,38 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     __builtin_amdgcn_sched_barrier(0);
 
     // ---- epilogue: O = O^T / l, one query row per lane ----------------------
-    const float inv = 1.f / half_swap_sum(l_i);
+    // (fp32 or bf16 rows; optionally the row's log-sum-exp, natural log:
+    // the reference m_i is in log2 units and includes the scale)
+    const float l_row = half_swap_sum(l_i);
+    const float inv = 1.f / l_row;
     if (qrow < Sq) {
-        float* orow = O + ((long long)bh * Sq + qrow) * D + 4 * hh;
+        const long long row = (long long)bh * Sq + qrow;
+        if (args.out_bf16) {
+            uint16_t* orow = static_cast<uint16_t*>(args.o) + row * D + 4 * hh;
 #pragma unroll
-        for (int cb = 0; cb < CB; ++cb)
+            for (int cb = 0; cb < CB; ++cb)
 #pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                float4 val = {oacc[cb][4 * g] * inv, oacc[cb][4 * g + 1] * inv,
-                              oacc[cb][4 * g + 2] * inv, oacc[cb][4 * g + 3] * inv};
-                *reinterpret_cast<float4*>(orow + cb * 32 + 8 * g) = val;
-            }
+                for (int g = 0; g < 4; ++g) {
+                    const bf16x2 lo = {(__bf16)(oacc[cb][4 * g] * inv),
+                                       (__bf16)(oacc[cb][4 * g + 1] * inv)};
+                    const bf16x2 hi = {(__bf16)(oacc[cb][4 * g + 2] * inv),
+                                       (__bf16)(oacc[cb][4 * g + 3] * inv)};
+                    const uint2 w = {__builtin_bit_cast(uint32_t, lo),
+                                     __builtin_bit_cast(uint32_t, hi)};
+                    *reinterpret_cast<uint2*>(orow + cb * 32 + 8 * g) = w;
+                }
+        } else {
+            float* orow = static_cast<float*>(args.o) + row * D + 4 * hh;
+#pragma unroll
+            for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    float4 val = {oacc[cb][4 * g] * inv, oacc[cb][4 * g + 1] * inv,
+                                  oacc[cb][4 * g + 2] * inv, oacc[cb][4 * g + 3] * inv};
+                    *reinterpret_cast<float4*>(orow + cb * 32 + 8 * g) = val;
+                }
+        }
+        if (args.lse && hh == 0) args.lse[row] = (m_i + __builtin_log2f(l_row)) * kLn2;
     }
     // Pipes 0, 1 and 3 end every tile with a barrier, after which no wave
     // reads LDS, so the next q-tile may refill the slots at once; the

@@ -246,12 +246,25 @@ int plan_fwd_all(const attn_device_desc& desc, int B, int H, int Sq, int Skv, in
     return n;
 }
 
-bool plan_decode(const attn_device_desc& desc, int B, int H, int Skv, int d, int n_req,
+// Query heads per decode workgroup: the largest of 8, 4, 2, 1 dividing the
+// number of query heads that share a key/value head.
+int decode_heads_per_wg(int group) {
+    for (int gq : {8, 4, 2})
+        if (group % gq == 0) return gq;
+    return 1;
+}
+
+bool plan_decode(const attn_device_desc& desc, int B, int Hq, int Hkv, int Skv, int d, int n_req,
                  DecodePlan* out) {
-    const int nt = kDecodeThreads, unroll = kDecodeUnroll;
+    if (Hkv <= 0 || Hq % Hkv != 0) return false;
+    // query heads sharing a key/value head run in one workgroup, which reads
+    // each K/V chunk once for all of them
+    const int gq = decode_heads_per_wg(Hq / Hkv);
+    const int nt = kDecodeThreads, unroll = gq >= 4 ? 4 : kDecodeUnroll;
     const int groups = nt / (d / 8);       // keys per workgroup step
     const int step_keys = groups * unroll;  // keys per loop iteration
-    const long long BH = (long long)B * H;
+    const long long BH = (long long)B * Hq / gq;  // key/value streams
+    const long long BHq = (long long)B * Hq;
     const double cu_share = desc.hbm_bytes_per_s / desc.num_cus;  // bytes/s per CU
     const int max_wg_cu = std::max(1, desc.max_waves_per_simd * desc.simds_per_cu / (nt / 64));
 
@@ -270,7 +283,7 @@ bool plan_decode(const attn_device_desc& desc, int B, int H, int Skv, int d, int
         const double steps = ceil((double)chunk / step_keys);
         const double stream_us = per_cu * wg_bytes / cu_bw * 1e6;
         const double merge_us = ceil(per_cu / resident) * 1.0;  // LDS merge + write, ~1 us
-        const double combine_bytes = (double)BH * n_eff * (d + 2) * 4.0 + BH * d * 4.0;
+        const double combine_bytes = (double)BHq * n_eff * (d + 2) * 4.0 + BHq * d * 4.0;
         const double combine_us = desc.launch_us + combine_bytes / desc.hbm_bytes_per_s * 1e6 +
                                   n_eff * 0.01;
         p->d = d;
@@ -278,6 +291,7 @@ bool plan_decode(const attn_device_desc& desc, int B, int H, int Skv, int d, int
         p->chunk = chunk;
         p->threads = nt;
         p->unroll = unroll;
+        p->heads_per_wg = gq;
         p->wg_per_cu = (int)resident;
         p->grid = grid;
         p->modeled_us = desc.launch_us + stream_us + merge_us + combine_us;
@@ -329,9 +343,10 @@ int format_fwd_plan(const FwdPlan& p, char* buf, int buflen) {
 
 int format_decode_plan(const DecodePlan& p, char* buf, int buflen) {
     return snprintf(buf, buf ? (size_t)buflen : 0,
-                    "kind=decode d=%d N_SPLITS=%d CHUNK=%d THREADS=%d UNROLL=%d grid=%lld "
-                    "wg_per_cu=%d modeled_us=%.3f bound=%s",
-                    p.d, p.n_splits, p.chunk, p.threads, p.unroll, p.grid, p.wg_per_cu,
+                    "kind=decode d=%d N_SPLITS=%d CHUNK=%d THREADS=%d UNROLL=%d HEADS_PER_WG=%d "
+                    "grid=%lld wg_per_cu=%d modeled_us=%.3f bound=%s",
+                    p.d, p.n_splits, p.chunk, p.threads, p.unroll, p.heads_per_wg, p.grid,
+                    p.wg_per_cu,
                     p.modeled_us, p.bound);
 }
 

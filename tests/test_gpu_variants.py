@@ -1,0 +1,162 @@
+"""GPU parity of the path's variants (through the C ABI) against the fp64 oracle.
+
+Grouped-query heads (prefill and decode), bf16 output, the row log-sum-exp,
+and a caller-provided decode workspace.  Inputs are seeded bf16 N(0,1).
+Tolerances: outputs as the main parity tests (max-abs 2e-2, mean-abs 2e-3);
+the log-sum-exp within 5e-3 (the kernel's normaliser sums bf16-rounded
+probabilities, each within a relative 2^-8 of its exact value, so log l is
+within 2^-8 = 3.9e-3 of exact, plus fp32 accumulation of the scores).
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from attn_inputs import random_bf16
+from tests.gpu_common import announce, compare, forced_plan
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+LSE_MAX_ABS = 5e-3
+LSE_MEAN_ABS = 1e-3
+
+
+@pytest.fixture(scope="module")
+def pa():
+    import paper_2609_29219_amd as pa
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    return pa
+
+
+def _qkv(B, Hq, Hkv, Sq, Skv, d, seed):
+    return (random_bf16((B, Hq, Sq, d), seed), random_bf16((B, Hkv, Skv, d), seed + 1),
+            random_bf16((B, Hkv, Skv, d), seed + 2))
+
+
+GQA_SHAPES = [  # B, Hq, Hkv, Sq, Skv, d, causal
+    (2, 4, 2, 77, 130, 128, False),
+    (1, 8, 2, 200, 200, 128, True),
+    (1, 6, 1, 65, 300, 64, False),
+    (2, 8, 8, 130, 130, 64, True),
+    (1, 16, 2, 33, 257, 128, True),
+]
+
+
+@pytest.mark.parametrize("shape", GQA_SHAPES, ids=[str(s) for s in GQA_SHAPES])
+def test_fwd_gqa_lse(pa, shape):
+    B, Hq, Hkv, Sq, Skv, d, causal = shape
+    q, k, v = _qkv(B, Hq, Hkv, Sq, Skv, d, 700 + Hq + Sq)
+    sc = float(np.float32(1.0 / math.sqrt(d)))
+    announce(f"attn_fwd_ex gqa {shape}")
+    o, lse = pa.attn_fwd(q.to(DEV), k.to(DEV), v.to(DEV), scale=sc, causal=causal,
+                         return_lse=True)
+    torch.cuda.synchronize()
+    ref, ref_lse = oracle.attn_gqa(q, k, v, B, Hq, Hkv, Sq, Skv, d, sc, causal)
+    compare(o, ref, f"gqa out {shape}")
+    compare(lse, ref_lse, f"gqa lse {shape}", max_abs=LSE_MAX_ABS, mean_abs=LSE_MEAN_ABS)
+
+
+@pytest.mark.parametrize("variant", [(64, 8, 1), (128, 8, 1), (64, 4, 0), (64, 8, 2), (64, 8, 3),
+                                     (32, 4, 3)])
+def test_fwd_gqa_every_schedule(pa, variant):
+    B, Hq, Hkv, Sq, Skv, d = 1, 8, 2, 290, 290, 128
+    q, k, v = _qkv(B, Hq, Hkv, Sq, Skv, d, 800)
+    sc = float(np.float32(1.0 / math.sqrt(d)))
+    with forced_plan(*variant):
+        for causal in (False, True):
+            announce(f"attn_fwd_ex gqa variant {variant} causal={causal}")
+            o, lse = pa.attn_fwd(q.to(DEV), k.to(DEV), v.to(DEV), scale=sc, causal=causal,
+                                 return_lse=True)
+            torch.cuda.synchronize()
+            ref, ref_lse = oracle.attn_gqa(q, k, v, B, Hq, Hkv, Sq, Skv, d, sc, causal)
+            compare(o, ref, f"variant {variant}")
+            compare(lse, ref_lse, f"variant {variant} lse", max_abs=LSE_MAX_ABS,
+                    mean_abs=LSE_MEAN_ABS)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_fwd_bf16_output_is_the_rounded_fp32_output(pa, causal):
+    B, H, Sq, Skv, d = 2, 3, 150, 150, 128
+    q, k, v = _qkv(B, H, H, Sq, Skv, d, 900)
+    qd, kd, vd = q.to(DEV), k.to(DEV), v.to(DEV)
+    announce(f"attn_fwd_ex bf16 output causal={causal}")
+    o32 = pa.attn_fwd(qd, kd, vd, causal=causal)
+    o16 = pa.attn_fwd(qd, kd, vd, causal=causal, out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    assert o16.dtype == torch.bfloat16
+    # same arithmetic, then round to nearest even: bit-exact
+    assert torch.equal(o16.cpu(), o32.cpu().to(torch.bfloat16))
+    ref = oracle.attn(q, k, v, B, H, Sq, Skv, d, float(np.float32(1 / math.sqrt(d))), causal)
+    compare(o16.float(), ref, "bf16 output")
+
+
+def test_fwd_lse_special_cases(pa):
+    # Q = 0: every allowed score is 0, lse = log(#allowed keys) (exact up to fp32)
+    B, H, Sq, Skv, d = 1, 2, 100, 160, 64
+    k, v = random_bf16((B, H, Skv, d), 950), random_bf16((B, H, Skv, d), 951)
+    q0 = torch.zeros((B, H, Sq, d), dtype=torch.bfloat16)
+    announce("attn_fwd_ex lse with Q = 0")
+    for causal in (False, True):
+        _, lse = pa.attn_fwd(q0.to(DEV), k.to(DEV), v.to(DEV), causal=causal, return_lse=True)
+        torch.cuda.synchronize()
+        n = np.full(Sq, Skv) if not causal else np.arange(Sq) + (Skv - Sq) + 1
+        np.testing.assert_allclose(lse.cpu().double().numpy(),
+                                   np.broadcast_to(np.log(n), (B, H, Sq)), atol=2e-6, rtol=0)
+
+
+def test_fwd_ex_rejects_before_launch(pa):
+    q = torch.zeros((1, 4, 8, 64), dtype=torch.bfloat16, device=DEV)
+    k = torch.zeros((1, 3, 8, 64), dtype=torch.bfloat16, device=DEV)
+    with pytest.raises(pa.AttnError) as e:
+        pa.attn_fwd(q, k, k)  # 3 key/value heads do not divide 4 query heads
+    assert e.value.code == pa.ATTN_EINVAL
+
+
+DECODE_GQA = [  # B, Hq, Hkv, Skv, d, n_splits
+    (2, 8, 2, 1000, 128, 0),
+    (1, 32, 4, 4096, 128, 0),
+    (3, 6, 2, 777, 64, 5),
+    (1, 16, 1, 2049, 128, 0),
+    (2, 12, 4, 300, 128, 3),
+    (1, 32, 2, 8192, 64, 0),
+]
+
+
+@pytest.mark.parametrize("shape", DECODE_GQA, ids=[str(s) for s in DECODE_GQA])
+def test_decode_gqa_lse(pa, shape):
+    B, Hq, Hkv, Skv, d, n = shape
+    q = random_bf16((B, Hq, d), 1000 + Hq)
+    k, v = random_bf16((B, Hkv, Skv, d), 1001 + Hq), random_bf16((B, Hkv, Skv, d), 1002 + Hq)
+    announce(f"attn_decode_ex gqa {shape}")
+    o, lse = pa.attn_decode(q.to(DEV), k.to(DEV), v.to(DEV), n_splits=n, return_lse=True)
+    torch.cuda.synchronize()
+    sc = float(np.float32(1.0 / math.sqrt(d)))
+    ref, ref_lse = oracle.attn_gqa(q.reshape(B, Hq, 1, d).contiguous(), k, v, B, Hq, Hkv, 1, Skv,
+                                   d, sc, False)
+    compare(o, ref.reshape(B, Hq, d), f"decode gqa {shape}")
+    # decode sums unrounded fp32 probabilities: the lse is fp32-accurate
+    compare(lse, ref_lse.reshape(B, Hq), f"decode gqa lse {shape}", max_abs=1e-4, mean_abs=2e-5)
+
+
+def test_decode_caller_workspace(pa):
+    B, Hq, Hkv, Skv, d = 2, 8, 2, 3000, 128
+    q = random_bf16((B, Hq, d), 1100).to(DEV)
+    k, v = random_bf16((B, Hkv, Skv, d), 1101).to(DEV), random_bf16((B, Hkv, Skv, d), 1102).to(DEV)
+    for n in (0, 7):
+        need = pa.decode_workspace_bytes(B, Hq, Hkv, Skv, d, n)
+        announce(f"attn_decode_ex caller workspace n={n} bytes={need}")
+        assert need > 0
+        ws = torch.empty(need, dtype=torch.uint8, device=DEV)
+        a = pa.attn_decode(q, k, v, n_splits=n)
+        b = pa.attn_decode(q, k, v, n_splits=n, workspace=ws)
+        torch.cuda.synchronize()
+        assert torch.equal(a.cpu(), b.cpu()), "caller workspace changes the result"
+        small = torch.empty(need - 16, dtype=torch.uint8, device=DEV)
+        with pytest.raises(pa.AttnError) as e:
+            pa.attn_decode(q, k, v, n_splits=n, workspace=small)
+        assert e.value.code == pa.ATTN_EINVAL
