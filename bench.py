@@ -235,7 +235,7 @@ def main():
                    "roofline": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS,
                                 "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS,
                                 "traffic": profiled_traffic("decode", wd.name),
-                                "kernel": "decode_partial_kernel + decode_combine_kernel",
+                                "kernel": "decode_partial_kernel + split_combine_kernel",
                                 "bytes_per_call": wd.hbm_bytes()}},
     }
     if not a.no_cpu_baseline:

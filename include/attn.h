@@ -44,7 +44,7 @@ extern "C" {
 #define ATTN_EINVAL (-1)       /* null or misaligned pointer, a dim <= 0, bad buffer length */
 #define ATTN_EUNSUPPORTED (-2) /* d not in {64,128}, causal with Sq > Skv, device not gfx950 */
 #define ATTN_EHIP (-3)         /* HIP runtime or launch error (message in attn_last_error) */
-#define ATTN_ENOMEM (-4)       /* decode workspace allocation failed */
+#define ATTN_ENOMEM (-4)       /* workspace allocation failed */
 
 #define ATTN_KIND_FWD 0
 #define ATTN_KIND_DECODE 1
@@ -79,6 +79,15 @@ int attn_fwd(const void* q, const void* k, const void* v, float* o, int B, int H
  *   lse_i = log sum_j exp(scale q_i.k_j), so softmax weights are
  *   exp(s_ij - lse_i) -- what a caller needs to merge partial attention
  *   results (split-KV, ring attention).
+ * Split keys: when the heads and q-tiles are too few to fill the device,
+ * the planner may split each head's keys (non-causal only) into chunks
+ * handled by separate workgroups, as Flash Decode splits its reduction
+ * dimension; their partial results (row max, sum, unnormalised output) go
+ * to the per-stream workspace described under attn_decode, and a combine
+ * kernel on the same stream writes o and lse.  Such a call may allocate or
+ * grow that workspace (ATTN_ENOMEM on failure); the result equals the
+ * unsplit one up to fp32 rounding.  attn_get_plan reports the choice
+ * (KV_SPLITS, KV_CHUNK).
  * Errors as attn_fwd; EINVAL also for Hkv not dividing Hq, unknown flags or
  * a misaligned lse; EUNSUPPORTED if one head's K or V exceeds 2 GiB.
  */
@@ -96,8 +105,8 @@ int attn_fwd_ex(const void* q, const void* k, const void* v, void* o, float* lse
  *   launched).  Every split count gives the same result up to fp32
  *   rounding.
  * Workspace: B*H*n*(d+2)*4 bytes of device memory that the library owns and
- * keeps per stream, reused by every later call on that stream (stream order
- * serialises them) until the process ends.  A call that needs more than the
+ * keeps per stream, reused by every later call on that stream (decode and
+ * split-key prefill; stream order serialises them) until the process ends.  A call that needs more than the
  * stream's current workspace drains that stream once, frees it and allocates
  * the next power of two; ATTN_ENOMEM if that allocation fails.  No other
  * call allocates or synchronises.
@@ -190,8 +199,8 @@ int attn_measure_device(attn_device_desc* out);
 
 /*
  * Plan query: writes a one-line, human-readable plan -- the named tile
- * symbols (BLOCK_M, BLOCK_N, WAVES, DBUF for ATTN_KIND_FWD; N_SPLITS, CHUNK,
- * ... for ATTN_KIND_DECODE), the grid size, the modelled time in us and the
+ * symbols (BLOCK_M, BLOCK_N, WAVES, PIPE, KV_SPLITS, KV_CHUNK for
+ * ATTN_KIND_FWD; N_SPLITS, CHUNK, ... for ATTN_KIND_DECODE), the grid size, the modelled time in us and the
  * binding resource -- for the given problem into buf (NUL-terminated,
  * truncated to buflen).  Returns the full length of the line (excluding the
  * NUL) or a negative ATTN_E* code.  Sq is ignored for decode.  desc may be

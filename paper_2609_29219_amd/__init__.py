@@ -241,10 +241,10 @@ def fwd_candidates(B: int, H: int, Sq: int, Skv: int, d: int, causal: bool = Fal
     the block-size ablation).  desc None: this device's description and the
     compiled kernels' real register/occupancy footprint; with a desc, the
     footprint is estimated unless device_footprint is set."""
-    buf = ctypes.create_string_buffer(1 << 16)
+    buf = ctypes.create_string_buffer(1 << 18)
     ptr = ctypes.byref(desc) if desc is not None else None
     rc = lib.attn__fwd_candidates(ptr, B, H, Sq, Skv, d, int(bool(causal)),
-                                  int(bool(device_footprint)), buf, 1 << 16)
+                                  int(bool(device_footprint)), buf, 1 << 18)
     if rc < 0:
         raise AttnError(rc, last_error())
     return [parse_plan(l) for l in buf.value.decode().splitlines() if l.strip()]

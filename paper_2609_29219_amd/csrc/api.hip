@@ -37,8 +37,8 @@ bool fwd_resources_forced(int d, int bn, int waves, int pipe, int causal, Kernel
 }
 
 hipError_t launch_fwd(const FwdPlan& p, const void* q, const void* k, const void* v, void* o,
-                      float* lse, int group, int out_bf16, int Sq, int Skv, float scale,
-                      int num_xcds, hipStream_t stream) {
+                      float* lse, int group, int out_bf16, long long rows, int Sq, int Skv,
+                      float scale, int num_xcds, float* workspace, hipStream_t stream) {
     // softmax in base 2: exp(x) = 2^(x*log2 e); a negative scale is applied
     // as an exact sign flip of Q.  The kernel needs a factor > 0 (masked
     // scores are -inf); a zero scale becomes the smallest normal float, with
@@ -60,9 +60,21 @@ hipError_t launch_fwd(const FwdPlan& p, const void* q, const void* k, const void
     a.out_bf16 = out_bf16;
     a.scale_log2 = (float)s;
     a.q_sign = scale < 0.f ? 0x80008000u : 0u;
-    if (p.d == 64) return launch_fwd_d64(p, a, stream);
-    if (p.d == 128) return launch_fwd_d128(p, a, stream);
-    return hipErrorInvalidValue;
+    const int n = p.kv_splits;
+    a.kv_splits = n;
+    a.kv_chunk = n > 1 ? p.kv_chunk : Skv;
+    // partial outputs first: their rows of d floats stay 16-byte aligned
+    a.ws_o = n > 1 ? workspace : nullptr;
+    a.ws_m = n > 1 ? workspace + rows * n * p.d : nullptr;
+    a.ws_l = n > 1 ? a.ws_m + rows * n : nullptr;
+    if (n > 1 && (p.causal || p.pipe == 2 || !workspace || p.kv_chunk % p.block_n != 0 ||
+                  (long long)(n - 1) * p.kv_chunk >= Skv))
+        return hipErrorInvalidValue;
+    hipError_t e = hipErrorInvalidValue;
+    if (p.d == 64) e = launch_fwd_d64(p, a, stream);
+    if (p.d == 128) e = launch_fwd_d128(p, a, stream);
+    if (e != hipSuccess || n == 1) return e;
+    return launch_split_combine(p.d, a.ws_m, a.ws_l, a.ws_o, o, out_bf16, lse, rows, n, stream);
 }
 }  // namespace attn
 
@@ -147,11 +159,43 @@ int device_state(DeviceState** out) {
 }
 
 // Optional fixed tile choice for the block-size ablation only:
-// ATTN_FORCE_PLAN="bn=64,waves=8,pipe=2".  Never used to select tiles.
-bool forced_fwd(int* bn, int* waves, int* pipe) {
+// ATTN_FORCE_PLAN="bn=64,waves=8,pipe=2" (optionally ",splits=4").  Never
+// used to select tiles.
+bool forced_fwd(int* bn, int* waves, int* pipe, int* splits) {
     const char* s = getenv("ATTN_FORCE_PLAN");
     if (!s || !*s) return false;
-    return sscanf(s, "bn=%d,waves=%d,pipe=%d", bn, waves, pipe) == 3;
+    *splits = 1;
+    const int n = sscanf(s, "bn=%d,waves=%d,pipe=%d,splits=%d", bn, waves, pipe, splits);
+    return n == 3 || n == 4;
+}
+
+// The per-stream workspace (decode partials, split-key prefill partials) of
+// at least bytes bytes.  Calls on one stream are serialised by the stream,
+// so they share one buffer.
+int stream_workspace(DeviceState* st, size_t bytes, void** out) {
+    std::lock_guard<std::mutex> lk(g_mu);
+    Workspace& w = st->ws[t_stream];
+    if (w.bytes < bytes) {
+        // grow to the next power of two; the old buffer may still be in use
+        // by work queued on this stream, so drain the stream first (rare)
+        size_t want = 4096;
+        while (want < bytes) want *= 2;
+        if (w.ptr) {
+            hipError_t e = hipStreamSynchronize(t_stream);
+            if (e == hipSuccess) e = hipFree(w.ptr);
+            if (e != hipSuccess) return fail_hip(e, "workspace release");
+            w = Workspace{};
+        }
+        hipError_t e = hipMalloc(&w.ptr, want);
+        if (e != hipSuccess || !w.ptr) {
+            (void)hipGetLastError();
+            w = Workspace{};
+            return fail(ATTN_ENOMEM, "workspace of %zu bytes: %s", want, hipGetErrorString(e));
+        }
+        w.bytes = want;
+    }
+    *out = w.ptr;
+    return ATTN_OK;
 }
 
 int validate_common(const void* q, const void* k, const void* v, const void* o, int B, int H,
@@ -258,8 +302,10 @@ int attn__fwd_candidates(const attn_device_desc* desc, int B, int H, int Sq, int
     if (buflen < 0 || (buflen > 0 && !buf)) return fail(ATTN_EINVAL, "bad output buffer");
     if (B <= 0 || H <= 0 || Sq <= 0 || Skv <= 0) return fail(ATTN_EINVAL, "bad dimensions");
     if (d != 64 && d != 128) return fail(ATTN_EUNSUPPORTED, "head dim %d not in {64, 128}", d);
-    FwdPlan plans[64];
-    const int n = std::min(64, plan_fwd_all(*desc, B, H, Sq, Skv, d, causal ? 1 : 0, plans, 64, res));
+    constexpr int kCap = 512;
+    std::vector<FwdPlan> plans(kCap);
+    const int n = std::min(kCap, plan_fwd_all(*desc, B, H, Sq, Skv, d, causal ? 1 : 0,
+                                              plans.data(), kCap, res));
     int len = 0;
     for (int i = 0; i < n; ++i) {
         char line[512];
@@ -301,10 +347,10 @@ int attn_fwd_ex(const void* q, const void* k, const void* v, void* o, float* lse
 
     const int c = causal ? 1 : 0;
     FwdPlan plan;
-    int fbn, fw, fpipe;
-    if (forced_fwd(&fbn, &fw, &fpipe)) {
+    int fbn, fw, fpipe, fsplits;
+    if (forced_fwd(&fbn, &fw, &fpipe, &fsplits)) {
         if (!plan_fwd_fixed(st->desc, B, Hq, Sq, Skv, d, c, fbn, fw, fpipe, &plan,
-                            fwd_resources_forced))
+                            fwd_resources_forced, fsplits))
             return fail(ATTN_EINVAL, "ATTN_FORCE_PLAN names an infeasible or unknown tile");
     } else {
         std::lock_guard<std::mutex> lk(g_mu);
@@ -318,8 +364,15 @@ int attn_fwd_ex(const void* q, const void* k, const void* v, void* o, float* lse
             g_fwd_cache[key] = plan;
         }
     }
+    const long long rows = (long long)B * Hq * Sq;
+    void* ws = nullptr;
+    if (plan.kv_splits > 1) {
+        rc = stream_workspace(st, (size_t)fwd_workspace_bytes(plan, rows), &ws);
+        if (rc) return rc;
+    }
     hipError_t e = launch_fwd(plan, q, k, v, o, lse, Hq / Hkv, (flags & ATTN_OUT_BF16) ? 1 : 0,
-                              Sq, Skv, scale, st->desc.num_xcds, t_stream);
+                              rows, Sq, Skv, scale, st->desc.num_xcds, static_cast<float*>(ws),
+                              t_stream);
     if (e != hipSuccess) return fail_hip(e, "prefill launch");
     return ATTN_OK;
 }
@@ -388,29 +441,8 @@ int attn_decode_ex(const void* q, const void* k, const void* v, float* o, float*
             return fail(ATTN_EINVAL, "workspace of %zu bytes, %zu needed", workspace_bytes,
                         ws_bytes);
     } else {
-        std::lock_guard<std::mutex> lk(g_mu);
-        Workspace& w = st->ws[t_stream];
-        if (w.bytes < ws_bytes) {
-            // grow to the next power of two; the old buffer may still be in use
-            // by work queued on this stream, so drain the stream first (rare)
-            size_t want = 4096;
-            while (want < ws_bytes) want *= 2;
-            if (w.ptr) {
-                hipError_t e = hipStreamSynchronize(t_stream);
-                if (e == hipSuccess) e = hipFree(w.ptr);
-                if (e != hipSuccess) return fail_hip(e, "decode workspace release");
-                w = Workspace{};
-            }
-            hipError_t e = hipMalloc(&w.ptr, want);
-            if (e != hipSuccess || !w.ptr) {
-                (void)hipGetLastError();
-                w = Workspace{};
-                return fail(ATTN_ENOMEM, "decode workspace of %zu bytes: %s", want,
-                            hipGetErrorString(e));
-            }
-            w.bytes = want;
-        }
-        ws = w.ptr;
+        rc = stream_workspace(st, ws_bytes, &ws);
+        if (rc) return rc;
     }
     const float scale = (float)(1.0 / sqrt((double)d));
     const hipError_t e = launch_decode(plan, q, k, v, o, lse, static_cast<float*>(ws), B, Hq,

@@ -23,6 +23,8 @@ struct FwdPlan {
     int wg_per_cu = 0;  // modelled occupancy
     long long grid = 0;
     int n_qtiles = 0;
+    int kv_splits = 1;  // key splits per head (non-causal only), with a combine kernel
+    int kv_chunk = 0;   // keys per split (a multiple of block_n; Skv when unsplit)
     double modeled_us = 0.0;
     const char* bound = "";  // resource that binds the modelled time
 };
@@ -69,6 +71,16 @@ struct FwdArgs {
     int out_bf16;
     float scale_log2;   // |scale| * log2(e), > 0
     uint32_t q_sign;    // sign bits xor-ed into Q (negative scale)
+    // Split key range (non-causal): kv_splits > 1 gives each workgroup the keys
+    // [s*kv_chunk, min(Skv, (s+1)*kv_chunk)) of split s, and it writes the
+    // unnormalised partials of each row r to index r*kv_splits + s of ws_m
+    // (running max, log2 units with the scale), ws_l (sum) and ws_o (d values)
+    // instead of o and lse; the split combine then produces o and lse.
+    int kv_splits;      // 1: direct output
+    int kv_chunk;       // keys per split, a multiple of the tile width (Skv if 1 split)
+    float* ws_m;
+    float* ws_l;
+    float* ws_o;
 };
 
 // Resource usage of one compiled prefill variant, as the runtime reports it:
@@ -88,7 +100,15 @@ bool plan_fwd(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d
               FwdPlan* out, FwdResFn res = nullptr);
 bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d,
                     int causal, int bn, int waves, int pipe, FwdPlan* out,
-                    FwdResFn res = nullptr);
+                    FwdResFn res = nullptr, int kv_splits = 1);
+// Key-split counts tried for non-causal prefill (each must leave every split
+// non-empty with a chunk that is a multiple of the tile width).
+constexpr int kFwdKvSplits[] = {1, 2, 3, 4, 6, 8, 12, 16, 24, 32};
+// Bytes of the split-KV workspace: rows * splits * (d + 2) floats (the
+// partial outputs, then the maxima, then the sums).
+inline long long fwd_workspace_bytes(const FwdPlan& p, long long rows) {
+    return p.kv_splits > 1 ? rows * p.kv_splits * (p.d + 2) * 4LL : 0;
+}
 // Every feasible candidate (in the planner's search order), up to cap of them
 // into out; returns how many there are.
 int plan_fwd_all(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d, int causal,
@@ -102,9 +122,16 @@ int format_decode_plan(const DecodePlan& p, char* buf, int buflen);
 hipError_t measure_device(attn_device_desc* d);
 
 // Launchers (defined next to the kernels).
+// With p.kv_splits > 1, workspace holds fwd_workspace_bytes(p, B*Hq*Sq) bytes
+// and a split combine follows the prefill kernel on the same stream.
 hipError_t launch_fwd(const FwdPlan& p, const void* q, const void* k, const void* v, void* o,
-                      float* lse, int group, int out_bf16, int Sq, int Skv, float scale,
-                      int num_xcds, hipStream_t stream);
+                      float* lse, int group, int out_bf16, long long rows, int Sq, int Skv,
+                      float scale, int num_xcds, float* workspace, hipStream_t stream);
+// o[r] = sum_s 2^(m_rs - M) o_rs / sum_s 2^(m_rs - M) l_rs for each of rows rows
+// (M = max_s m_rs), fp32 or bf16, and optionally lse[r]; partials at r*n + s.
+hipError_t launch_split_combine(int d, const float* ws_m, const float* ws_l, const float* ws_o,
+                                void* o, int out_bf16, float* lse, long long rows, int n_splits,
+                                hipStream_t stream);
 hipError_t launch_decode(const DecodePlan& p, const void* q, const void* k, const void* v,
                          float* o, float* lse, float* workspace, int B, int Hq, int Hkv, int Skv,
                          float scale, hipStream_t stream);

@@ -5,7 +5,7 @@
 // of the latency-modelling section): a local softmax loop per chunk, a
 // gather of the partial results, a global softmax over them and the final
 // output.  Here the local loop is decode_partial_kernel and the gather +
-// global softmax + final output is decode_combine_kernel.
+// global softmax + final output is split_combine_kernel.
 //
 // decode_partial_kernel.  The work is a stream over K and V (HBM bound: 4*d
 // bytes per key against 4*d flops).  G = d/8 lanes share one key: each lane
@@ -163,17 +163,19 @@ __global__ __launch_bounds__(NT) void decode_partial_kernel(
 //   M = max_s m_s, w_s = 2^(m_s - M), o = sum_s w_s o_s / sum_s w_s l_s,
 // and optionally the log-sum-exp of the row's scores (natural log),
 //   lse = (M + log2(sum_s w_s l_s)) * ln 2.
+// One workgroup of D threads per row; the partials of row r are at r*n + s.
+// Used by decode and by split-key prefill (fp32 or bf16 output).
 template <int D>
-__global__ __launch_bounds__(D) void decode_combine_kernel(const float* __restrict__ ws_m,
-                                                           const float* __restrict__ ws_l,
-                                                           const float* __restrict__ ws_o,
-                                                           float* __restrict__ O,
-                                                           float* __restrict__ lse, int n_splits) {
-    const long long bh = blockIdx.x;
+__global__ __launch_bounds__(D) void split_combine_kernel(const float* __restrict__ ws_m,
+                                                          const float* __restrict__ ws_l,
+                                                          const float* __restrict__ ws_o,
+                                                          void* __restrict__ O, int out_bf16,
+                                                          float* __restrict__ lse, int n_splits) {
+    const long long r = blockIdx.x;
     const int c = threadIdx.x;
-    const float* mm = ws_m + bh * n_splits;
-    const float* ll = ws_l + bh * n_splits;
-    const float* oo = ws_o + bh * n_splits * D + c;
+    const float* mm = ws_m + r * n_splits;
+    const float* ll = ws_l + r * n_splits;
+    const float* oo = ws_o + r * n_splits * D + c;
     float M = -INFINITY;
     for (int s = 0; s < n_splits; ++s) M = fmaxf(M, mm[s]);
     float L = 0.f, acc = 0.f;
@@ -182,8 +184,28 @@ __global__ __launch_bounds__(D) void decode_combine_kernel(const float* __restri
         L = fmaf(w, ll[s], L);
         acc = fmaf(w, oo[(long long)s * D], acc);
     }
-    O[bh * D + c] = acc / L;
-    if (lse && c == 0) lse[bh] = (M + __builtin_log2f(L)) * 0.69314718055994531f;
+    const float val = acc / L;
+    if (out_bf16)
+        static_cast<__bf16*>(O)[r * D + c] = (__bf16)val;
+    else
+        static_cast<float*>(O)[r * D + c] = val;
+    if (lse && c == 0) lse[r] = (M + __builtin_log2f(L)) * 0.69314718055994531f;
+}
+
+hipError_t launch_split_combine(int d, const float* ws_m, const float* ws_l, const float* ws_o,
+                                void* o, int out_bf16, float* lse, long long rows, int n_splits,
+                                hipStream_t st) {
+    // one workgroup of d threads per row; a grid holds at most 2^32 - 1 threads
+    if (rows <= 0 || rows * d > 0xffffffffLL) return hipErrorInvalidValue;
+    if (d == 64)
+        hipLaunchKernelGGL((split_combine_kernel<64>), dim3((unsigned)rows), dim3(64), 0, st,
+                           ws_m, ws_l, ws_o, o, out_bf16, lse, n_splits);
+    else if (d == 128)
+        hipLaunchKernelGGL((split_combine_kernel<128>), dim3((unsigned)rows), dim3(128), 0, st,
+                           ws_m, ws_l, ws_o, o, out_bf16, lse, n_splits);
+    else
+        return hipErrorInvalidValue;
+    return hipGetLastError();
 }
 
 template <int D, int GQ>
@@ -218,9 +240,7 @@ static hipError_t launch_decode_d(const DecodePlan& p, const void* q, const void
         default: e = launch_partial<D, 1>(p, q, k, v, ws_m, ws_l, ws_o, BHq, Skv, group, scale_log2, st);
     }
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((decode_combine_kernel<D>), dim3((unsigned)BHq), dim3(D), 0, st, ws_m, ws_l,
-                       ws_o, o, lse, p.n_splits);
-    return hipGetLastError();
+    return launch_split_combine(D, ws_m, ws_l, ws_o, o, 0, lse, BHq, p.n_splits, st);
 }
 
 hipError_t launch_decode(const DecodePlan& p, const void* q, const void* k, const void* v,

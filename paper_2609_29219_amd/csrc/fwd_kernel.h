@@ -137,7 +137,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     const uint16_t* __restrict__ Q = args.q;
     const uint16_t* __restrict__ K = args.k;
     const uint16_t* __restrict__ V = args.v;
-    const int Sq = args.Sq, Skv = args.Skv, n_qtiles = args.n_qtiles, n_wg = args.n_wg;
+    const int Sq = args.Sq, n_qtiles = args.n_qtiles, n_wg = args.n_wg;
     const int num_xcds = args.num_xcds;
     const float scale_log2 = args.scale_log2;
     const uint32_t q_sign = args.q_sign;
@@ -175,14 +175,22 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
         (xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per) + slot_id;
     // Causal work grows linearly with the q-tile index, so a causal
     // workgroup takes the pair of q-tiles (n-1-u, u): every workgroup then
-    // holds n+1 tiles of work (heavy one first).  Non-causal: one q-tile.
+    // holds n+1 tiles of work (heavy one first).  Non-causal: one q-tile,
+    // of one key split (logical = (head, split, q-tile), q-tile fastest, so
+    // the workgroups reading one K/V chunk are neighbours on one XCD).
     const int units = CAUSAL ? (n_qtiles + 1) / 2 : n_qtiles;
-    const int bh = logical / units;
-    const int unit = logical % units;
+    const int kv_splits = (CAUSAL || PIPE == 2) ? 1 : args.kv_splits;
+    const int bh = logical / (units * kv_splits);
+    const int within = logical - bh * units * kv_splits;
+    const int split = within / units;
+    const int unit = within - split * units;
     const int n_pass = (CAUSAL && n_qtiles - 1 - unit != unit) ? 2 : 1;
+    // this workgroup's keys: [k0, k0 + Skv) of the head's args.Skv keys
+    const int k0 = split * args.kv_chunk;
+    const int Skv = CAUSAL ? args.Skv : min(args.kv_chunk, args.Skv - k0);
     const int diag = Skv - Sq;  // causal: key j allowed iff j <= row + diag
     // grouped-query heads: query head bh reads key/value head bh / group
-    const long long kv_base = (long long)(bh / args.group) * Skv * D;
+    const long long kv_base = ((long long)(bh / args.group) * args.Skv + k0) * D;
     const uint16_t* Kb = K + kv_base;
     const uint16_t* Vb = V + kv_base;
 
@@ -713,11 +721,16 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     // ---- epilogue: O = O^T / l, one query row per lane ----------------------
     // (fp32 or bf16 rows; optionally the row's log-sum-exp, natural log:
     // the reference m_i is in log2 units and includes the scale)
+    // With split keys the row's unnormalised partials (m_i, l, O) go to the
+    // workspace instead (the split combine normalises).
     const float l_row = half_swap_sum(l_i);
-    const float inv = 1.f / l_row;
+    // (not with the ping-pong schedule, which has no registers to spare)
+    const bool partial = PIPE != 2 && kv_splits > 1;
+    const float inv = partial ? 1.f : 1.f / l_row;
     if (qrow < Sq) {
         const long long row = (long long)bh * Sq + qrow;
-        if (args.out_bf16) {
+        const long long prow = row * kv_splits + split;  // == row when not split
+        if (args.out_bf16 && !partial) {
             uint16_t* orow = static_cast<uint16_t*>(args.o) + row * D + 4 * hh;
 #pragma unroll
             for (int cb = 0; cb < CB; ++cb)
@@ -732,7 +745,8 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
                     *reinterpret_cast<uint2*>(orow + cb * 32 + 8 * g) = w;
                 }
         } else {
-            float* orow = static_cast<float*>(args.o) + row * D + 4 * hh;
+            float* const obase = partial ? args.ws_o : static_cast<float*>(args.o);
+            float* orow = obase + prow * D + 4 * hh;
 #pragma unroll
             for (int cb = 0; cb < CB; ++cb)
 #pragma unroll
@@ -742,7 +756,11 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
                     *reinterpret_cast<float4*>(orow + cb * 32 + 8 * g) = val;
                 }
         }
-        if (args.lse && hh == 0) args.lse[row] = (m_i + __builtin_log2f(l_row)) * kLn2;
+        if (hh == 0) {
+            float* const mdst = partial ? args.ws_m : args.lse;
+            if (mdst) mdst[prow] = partial ? m_i : (m_i + __builtin_log2f(l_row)) * kLn2;
+            if (partial) args.ws_l[prow] = l_row;
+        }
     }
     // Pipes 0, 1 and 3 end every tile with a barrier, after which no wave
     // reads LDS, so the next q-tile may refill the slots at once; the

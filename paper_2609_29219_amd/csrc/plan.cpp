@@ -110,8 +110,17 @@ int fwd_vgprs(int d, int bn, int waves, int pipe) {
 // load/body boundary the pipe knob opens (pipe >= 1, Eq. heg-pipe): with pipe
 // 0 the load latency is exposed, shared by the g resident workgroups.  A
 // q-tile adds one exposed latency (Q and the first tile) to its loop.
+//
+// Split keys (non-causal, not with the ping-pong schedule; the Flash Decode
+// split of the reduction dimension, Evaluation, applied to prefill): with n
+// splits every (head, q-tile) becomes n workgroups over chunks of ceil(Skv/n) keys rounded up to whole
+// tiles, which fills the CUs when B*H*q-tiles is small; the price is Q read n
+// times, the partials (d + 2 floats per row and split) written and read back,
+// and a second launch (the split combine, the same global-softmax step as
+// decode's).
 bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d,
-                    int causal, int bn, int waves, int pipe, FwdPlan* out, FwdResFn res) {
+                    int causal, int bn, int waves, int pipe, FwdPlan* out, FwdResFn res,
+                    int kv_splits) {
     FwdPlan p;
     p.d = d;
     p.block_n = bn;
@@ -142,8 +151,19 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
     if (wg < 1) return false;
     p.wg_per_cu = wg;
     p.n_qtiles = (Sq + p.block_m - 1) / p.block_m;
+    // key splits: every split non-empty, chunks of whole tiles
+    if (kv_splits < 1 || (kv_splits > 1 && (causal || pipe == 2))) return false;
+    const long long rows = (long long)B * H * Sq;
+    p.kv_splits = kv_splits;
+    p.kv_chunk = Skv;
+    if (kv_splits > 1) {
+        const int per = (Skv + kv_splits - 1) / kv_splits;
+        p.kv_chunk = (per + bn - 1) / bn * bn;
+        if ((Skv + p.kv_chunk - 1) / p.kv_chunk != kv_splits) return false;
+        if (rows * d > 0xffffffffLL) return false;  // one combine workgroup per row
+    }
     // causal workgroups take q-tile pairs (n-1-u, u)
-    p.grid = (long long)B * H * (causal ? (p.n_qtiles + 1) / 2 : p.n_qtiles);
+    p.grid = (long long)B * H * (causal ? (p.n_qtiles + 1) / 2 : (long long)p.n_qtiles * kv_splits);
     if (p.grid > 0x7fffffffLL) return false;
 
     const double mfma_cyc = 32768.0 / (desc.mfma_bf16_flops_per_clk_cu / simds);
@@ -164,11 +184,11 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
 
     // ---- grid: regular (non-causal) or regularised (causal) --------------
     const double slots = (double)desc.num_cus * wg;
-    const int full_tiles = (Skv + bn - 1) / bn;
+    const int chunk_tiles = (p.kv_chunk + bn - 1) / bn;
     double cycles;
     if (!causal) {
         const double rounds = ceil((double)p.grid / slots);
-        cycles = rounds * (load_q + heg_for(full_tiles, tile));
+        cycles = rounds * (load_q + heg_for(chunk_tiles, tile));
     } else {
         // workgroups take q-tile pairs (n-1-u, u), which regularises the
         // triangular work: per workgroup the sum of the pair's tile counts
@@ -190,8 +210,18 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
         cycles = std::max(rounds * sum / units, longest);
     }
     double us = cycles / (desc.clock_ghz * 1e3);
-    const double bytes = (double)B * H * ((double)Sq * d * 6.0 + (double)Skv * d * 4.0);
+    // Q read once per split, K/V once, O (or the partials) written once
+    const double part_bytes = kv_splits > 1 ? (double)rows * kv_splits * (d + 2) * 4.0 : 0.0;
+    const double bytes = (double)B * H * ((double)Sq * d * 2.0 * kv_splits + (double)Skv * d * 4.0) +
+                         (kv_splits > 1 ? part_bytes : (double)rows * d * 4.0);
     const double hbm_us = bytes / desc.hbm_bytes_per_s * 1e6;
+    // the split combine: a launch, two dependent memory round trips (the
+    // maxima, then the sums and outputs), the partials read and O written
+    const double combine_us =
+        kv_splits > 1 ? desc.launch_us + 2.0 * desc.hbm_latency_us +
+                            (part_bytes + (double)rows * d * 4.0) / desc.hbm_bytes_per_s * 1e6 +
+                            kv_splits * 0.01
+                      : 0.0;
     const char* bound;
     if (hbm_us > us) {
         us = hbm_us;
@@ -205,7 +235,7 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
     } else {
         bound = "valu";
     }
-    p.modeled_us = us + desc.launch_us;
+    p.modeled_us = us + desc.launch_us + combine_us;
     p.bound = bound;
     *out = p;
     return true;
@@ -217,16 +247,18 @@ bool plan_fwd(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d
     FwdPlan best;
     for (int bn : kFwdBlockN)
         for (int waves : kFwdWaves)
-            for (int pipe : kFwdPipe) {
-                FwdPlan p;
-                if (!plan_fwd_fixed(desc, B, H, Sq, Skv, d, causal, bn, waves, pipe, &p, res))
-                    continue;
-                // strict improvement keeps the first (smallest) candidate on ties
-                if (!found || p.modeled_us < best.modeled_us * (1.0 - 1e-9)) {
-                    best = p;
-                    found = true;
+            for (int pipe : kFwdPipe)
+                for (int ns : kFwdKvSplits) {
+                    FwdPlan p;
+                    if (!plan_fwd_fixed(desc, B, H, Sq, Skv, d, causal, bn, waves, pipe, &p, res,
+                                        ns))
+                        continue;
+                    // strict improvement keeps the first (smallest) candidate on ties
+                    if (!found || p.modeled_us < best.modeled_us * (1.0 - 1e-9)) {
+                        best = p;
+                        found = true;
+                    }
                 }
-            }
     if (found) *out = best;
     return found;
 }
@@ -236,13 +268,15 @@ int plan_fwd_all(const attn_device_desc& desc, int B, int H, int Sq, int Skv, in
     int n = 0;
     for (int bn : kFwdBlockN)
         for (int waves : kFwdWaves)
-            for (int pipe : kFwdPipe) {
-                FwdPlan p;
-                if (!plan_fwd_fixed(desc, B, H, Sq, Skv, d, causal, bn, waves, pipe, &p, res))
-                    continue;
-                if (n < cap) out[n] = p;
-                ++n;
-            }
+            for (int pipe : kFwdPipe)
+                for (int ns : kFwdKvSplits) {
+                    FwdPlan p;
+                    if (!plan_fwd_fixed(desc, B, H, Sq, Skv, d, causal, bn, waves, pipe, &p, res,
+                                        ns))
+                        continue;
+                    if (n < cap) out[n] = p;
+                    ++n;
+                }
     return n;
 }
 
@@ -284,8 +318,8 @@ bool plan_decode(const attn_device_desc& desc, int B, int Hq, int Hkv, int Skv, 
         const double stream_us = per_cu * wg_bytes / cu_bw * 1e6;
         const double merge_us = ceil(per_cu / resident) * 1.0;  // LDS merge + write, ~1 us
         const double combine_bytes = (double)BHq * n_eff * (d + 2) * 4.0 + BHq * d * 4.0;
-        const double combine_us = desc.launch_us + combine_bytes / desc.hbm_bytes_per_s * 1e6 +
-                                  n_eff * 0.01;
+        const double combine_us = desc.launch_us + 2.0 * desc.hbm_latency_us +
+                                  combine_bytes / desc.hbm_bytes_per_s * 1e6 + n_eff * 0.01;
         p->d = d;
         p->n_splits = n_eff;
         p->chunk = chunk;
@@ -335,10 +369,12 @@ namespace attn {
 
 int format_fwd_plan(const FwdPlan& p, char* buf, int buflen) {
     return snprintf(buf, buf ? (size_t)buflen : 0,
-                    "kind=fwd d=%d BLOCK_M=%d BLOCK_N=%d WAVES=%d PIPE=%d causal=%d grid=%lld "
-                    "n_qtiles=%d lds_bytes=%d vgprs=%d wg_per_cu=%d modeled_us=%.3f bound=%s",
-                    p.d, p.block_m, p.block_n, p.waves, p.pipe, p.causal, p.grid, p.n_qtiles,
-                    p.lds_bytes, p.vgprs, p.wg_per_cu, p.modeled_us, p.bound);
+                    "kind=fwd d=%d BLOCK_M=%d BLOCK_N=%d WAVES=%d PIPE=%d KV_SPLITS=%d "
+                    "KV_CHUNK=%d causal=%d grid=%lld n_qtiles=%d lds_bytes=%d vgprs=%d "
+                    "wg_per_cu=%d modeled_us=%.3f bound=%s",
+                    p.d, p.block_m, p.block_n, p.waves, p.pipe, p.kv_splits, p.kv_chunk,
+                    p.causal, p.grid, p.n_qtiles, p.lds_bytes, p.vgprs, p.wg_per_cu,
+                    p.modeled_us, p.bound);
 }
 
 int format_decode_plan(const DecodePlan& p, char* buf, int buflen) {

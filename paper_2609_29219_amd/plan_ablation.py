@@ -4,12 +4,13 @@
                                                  [--markdown FILE]
 
 For each workload every feasible prefill candidate (block sizes, waves,
-pipeline knob) is run through the ATTN_FORCE_PLAN hook and timed, and set
+pipeline knob, key splits) is run through the ATTN_FORCE_PLAN hook and timed, and set
 against the planner's modelled time: where the planner's pick ranks among the
 measured times, how far it is from the measured best, whether the best is in
 the modelled top five, the rank correlation of modelled and measured times,
 and the pick's rank among its legal one-step neighbours (block width one
-step up or down, the other wave count, the neighbouring pipeline knob).  The
+step up or down, the other wave count, the neighbouring pipeline knob, the
+neighbouring key-split count).  The
 paper validates its model the same way (top-k candidates and block-size
 neighbourhoods); measurement here validates, it never selects.
 
@@ -42,13 +43,17 @@ WORKLOADS = [
     ("b4_h16_s2048_d128_causal", 4, 16, 2048, 2048, 128, True),
     ("b4_h16_s2048_d64", 4, 16, 2048, 2048, 64, False),
     ("b8_h8_s1024_d128", 8, 8, 1024, 1024, 128, False),
+    # few heads / few queries against many keys: key splits fill the CUs
+    ("b1_h2_s8192_d128", 1, 2, 8192, 8192, 128, False),
+    ("b1_h32_q256_kv32768_d128", 1, 32, 256, 32768, 128, False),
 ]
+SPLITS = (1, 2, 3, 4, 6, 8, 12, 16, 24, 32)
 CALIBRATED = ("issue_cycles_per_score", "valu_mfma_overlap", "tile_sync_cycles",
               "tile_latency_cycles")
 
 
 def key(c: dict) -> tuple:
-    return (c["BLOCK_N"], c["WAVES"], c["PIPE"])
+    return (c["BLOCK_N"], c["WAVES"], c["PIPE"], c["KV_SPLITS"])
 
 
 def time_variant(w, variant, iters=10, reps=3) -> float:
@@ -63,8 +68,8 @@ def time_variant(w, variant, iters=10, reps=3) -> float:
         o = torch.empty((B, H, Sq, d), dtype=torch.float32, device="cuda")
         time_variant.cache = (name, q, k, v, o)
     _, q, k, v, o = time_variant.cache
-    bn, nw, pipe = variant
-    os.environ["ATTN_FORCE_PLAN"] = f"bn={bn},waves={nw},pipe={pipe}"
+    bn, nw, pipe, ns = variant
+    os.environ["ATTN_FORCE_PLAN"] = f"bn={bn},waves={nw},pipe={pipe},splits={ns}"
     try:
         for _ in range(3):
             pa.attn_fwd(q, k, v, o=o, causal=causal)
@@ -84,17 +89,14 @@ def time_variant(w, variant, iters=10, reps=3) -> float:
 
 
 def neighbours(pick: tuple, feasible: set) -> list:
-    bns, waves, pipes = (32, 64, 128), (4, 8), (0, 1, 2, 3)
-    bn, nw, pipe = pick
+    """Feasible candidates at most one step from pick in every symbol."""
+    domains = ((32, 64, 128), (4, 8), (0, 1, 2, 3), SPLITS)
     out = []
-    for b in bns:
-        for w in waves:
-            for p in pipes:
-                steps = (abs(bns.index(b) - bns.index(bn)) + (w != nw) + abs(p - pipe))
-                if 0 < steps and abs(bns.index(b) - bns.index(bn)) <= 1 and abs(p - pipe) <= 1 \
-                        and (b, w, p) in feasible:
-                    out.append((b, w, p))
-    return out
+    for c in feasible:
+        steps = [abs(dom.index(a) - dom.index(b)) for dom, a, b in zip(domains, c, pick)]
+        if max(steps) <= 1 and sum(steps) > 0:
+            out.append(c)
+    return sorted(out)
 
 
 def spearman(a, b) -> float:
@@ -167,7 +169,7 @@ def fit(data: dict) -> dict:
 
 
 def markdown(summaries: list, fitted: dict | None) -> str:
-    out = ["| workload | candidates | planner pick (BN, waves, pipe) | pick vs measured best | "
+    out = ["| workload | candidates | planner pick (BN, waves, pipe, splits) | pick vs measured best | "
            "pick's measured rank | best in model top-5 | Spearman | pick's rank among its "
            "neighbours |", "|---|---|---|---|---|---|---|---|"]
     for s in summaries:
@@ -199,7 +201,9 @@ def main():
     if a.load:
         with open(a.load) as f:
             raw = json.load(f)
-        data = {w: {tuple(map(int, k.split(","))): t for k, t in m.items()} for w, m in raw.items()}
+        # keys "bn,waves,pipe[,splits]" (measurements from before key splits: 1 split)
+        data = {w: {(tuple(map(int, k.split(","))) + (1,))[:4]: t for k, t in m.items()}
+                for w, m in raw.items()}
     summaries = []
     for w in WORKLOADS:
         cands = pa.fwd_candidates(*w[1:])
@@ -210,7 +214,8 @@ def main():
                 print(f"{w[0]} {key(c)} modelled {c['modeled_us']:.1f} us measured "
                       f"{meas[key(c)]:.1f} us", flush=True)
             data[w[0]] = meas
-        summaries.append(summarise(w, cands, data[w[0]]))
+        if w[0] in data:
+            summaries.append(summarise(w, cands, data[w[0]]))
     if a.save:
         with open(a.save, "w") as f:
             json.dump({w: {",".join(map(str, k)): t for k, t in m.items()} for w, m in data.items()},

@@ -1,7 +1,7 @@
 """GPU parity of the path's variants (through the C ABI) against the fp64 oracle.
 
 Grouped-query heads (prefill and decode), bf16 output, the row log-sum-exp,
-and a caller-provided decode workspace.  Inputs are seeded bf16 N(0,1).
+a caller-provided decode workspace, and prefill with split key ranges.  Inputs are seeded bf16 N(0,1).
 Tolerances: outputs as the main parity tests (max-abs 2e-2, mean-abs 2e-3);
 the log-sum-exp within 5e-3 (the kernel's normaliser sums bf16-rounded
 probabilities, each within a relative 2^-8 of its exact value, so log l is
@@ -160,3 +160,91 @@ def test_decode_caller_workspace(pa):
         with pytest.raises(pa.AttnError) as e:
             pa.attn_decode(q, k, v, n_splits=n, workspace=small)
         assert e.value.code == pa.ATTN_EINVAL
+
+
+# ---------------------------------------------------------------- key splits
+class forced_split_plan(forced_plan):
+    def __init__(self, bn: int, waves: int, pipe: int, splits: int):
+        super().__init__(bn, waves, pipe)
+        self.value += f",splits={splits}"
+
+
+SPLIT_VARIANTS = [(32, 4, 0, 3), (32, 8, 3, 5), (64, 4, 1, 2), (64, 8, 3, 4), (64, 8, 1, 6),
+                  (128, 8, 1, 3), (128, 4, 0, 2)]
+
+
+@pytest.mark.parametrize("variant", SPLIT_VARIANTS, ids=[str(v) for v in SPLIT_VARIANTS])
+def test_fwd_key_splits_every_schedule(pa, variant):
+    # ragged query tail, key count that leaves a short last split, grouped heads
+    B, Hq, Hkv, Sq, Skv = 2, 4, 2, 77, 1000
+    for d in (64, 128):
+        q, k, v = _qkv(B, Hq, Hkv, Sq, Skv, d, 1200 + d)
+        sc = float(np.float32(1.0 / math.sqrt(d)))
+        announce(f"attn_fwd_ex key splits {variant} d={d}")
+        with forced_split_plan(*variant):
+            o, lse = pa.attn_fwd(q.to(DEV), k.to(DEV), v.to(DEV), scale=sc, return_lse=True)
+            o16 = pa.attn_fwd(q.to(DEV), k.to(DEV), v.to(DEV), scale=sc,
+                              out_dtype=torch.bfloat16)
+        torch.cuda.synchronize()
+        ref, ref_lse = oracle.attn_gqa(q, k, v, B, Hq, Hkv, Sq, Skv, d, sc, False)
+        compare(o, ref, f"splits {variant} d={d}")
+        compare(o16.float(), ref, f"splits {variant} d={d} bf16")
+        assert torch.equal(o16.cpu(), o.cpu().to(torch.bfloat16))
+        compare(lse, ref_lse, f"splits {variant} d={d} lse", max_abs=LSE_MAX_ABS,
+                mean_abs=LSE_MEAN_ABS)
+
+
+def test_fwd_key_splits_one_key_in_last_split(pa):
+    # Skv = 2*64 + 1 with 3 splits of 64 keys: the last split holds one key
+    B, H, Sq, Skv, d = 1, 3, 130, 129, 128
+    q, k, v = _qkv(B, H, H, Sq, Skv, d, 1300)
+    sc = float(np.float32(1.0 / math.sqrt(d)))
+    announce("attn_fwd_ex key splits, one-key split")
+    with forced_split_plan(64, 8, 1, 3):
+        o = pa.attn_fwd(q.to(DEV), k.to(DEV), v.to(DEV), scale=sc)
+    torch.cuda.synchronize()
+    compare(o, oracle.attn(q, k, v, B, H, Sq, Skv, d, sc, False), "one-key split")
+
+
+def test_fwd_key_splits_chosen_by_the_planner(pa):
+    # few heads and queries against many keys: the planner splits the keys
+    B, H, Sq, Skv, d = 1, 2, 256, 12000, 128
+    plan = pa.parse_plan(pa.get_plan(pa.KIND_FWD, B, H, Sq, Skv, d, False))
+    announce(f"attn_fwd planner split {plan}")
+    assert plan["KV_SPLITS"] > 1, plan
+    q, k, v = _qkv(B, H, H, Sq, Skv, d, 1400)
+    sc = float(np.float32(1.0 / math.sqrt(d)))
+    o, lse = pa.attn_fwd(q.to(DEV), k.to(DEV), v.to(DEV), scale=sc, return_lse=True)
+    torch.cuda.synchronize()
+    ref, ref_lse = oracle.attn_gqa(q, k, v, B, H, H, Sq, Skv, d, sc, False)
+    compare(o, ref, "planner split")
+    compare(lse, ref_lse, "planner split lse", max_abs=LSE_MAX_ABS, mean_abs=LSE_MEAN_ABS)
+
+
+def test_fwd_key_splits_after_decode_share_the_workspace(pa):
+    # decode and split prefill on one stream reuse the per-stream workspace
+    B, H, Sq, Skv, d = 1, 2, 64, 5000, 64
+    q, k, v = _qkv(B, H, H, Sq, Skv, d, 1500)
+    qd = random_bf16((B, H, d), 1501)
+    sc = float(np.float32(1.0 / math.sqrt(d)))
+    announce("split prefill interleaved with decode")
+    kd, vd = k.to(DEV), v.to(DEV)
+    with forced_split_plan(64, 4, 1, 6):
+        outs = []
+        for _ in range(3):
+            outs.append(pa.attn_fwd(q.to(DEV), kd, vd, scale=sc))
+            dec = pa.attn_decode(qd.to(DEV), kd, vd)
+    torch.cuda.synchronize()
+    for o in outs[1:]:
+        assert torch.equal(o.cpu(), outs[0].cpu())
+    compare(outs[0], oracle.attn(q, k, v, B, H, Sq, Skv, d, sc, False), "split prefill")
+    ref_d = oracle.attn(qd.reshape(B, H, 1, d).contiguous(), k, v, B, H, 1, Skv, d, sc, False)
+    compare(dec, ref_d.reshape(B, H, d), "decode between")
+
+
+def test_fwd_key_splits_rejected_for_causal(pa):
+    q = torch.zeros((1, 1, 64, 64), dtype=torch.bfloat16, device=DEV)
+    with forced_split_plan(64, 8, 1, 2):
+        with pytest.raises(pa.AttnError) as e:
+            pa.attn_fwd(q, q, q, causal=True)
+    assert e.value.code == pa.ATTN_EINVAL

@@ -180,3 +180,53 @@ def test_calibrated_fields_out_of_range_rejected(field, value):
     with pytest.raises(pa.AttnError) as e:
         plan(d, pa.KIND_FWD, 1, 1, 64, 64, 64)
     assert e.value.code == pa.ATTN_EINVAL
+
+
+# ---------------------------------------------------------------- key splits
+SPLIT_SHAPES = [(1, 1, 256, 256, 64, False), (1, 2, 8192, 8192, 128, False),
+                (1, 32, 256, 32768, 128, False), (2, 4, 1000, 3001, 64, False),
+                (1, 32, 8192, 8192, 128, False), (4, 16, 2048, 2048, 128, True)]
+
+
+@pytest.mark.parametrize("shape", SPLIT_SHAPES)
+def test_key_split_candidates_are_consistent(shape):
+    B, H, Sq, Skv, d, causal = shape
+    cands = pa.fwd_candidates(B, H, Sq, Skv, d, causal, desc=spec())
+    assert cands
+    for c in cands:
+        n, chunk = c["KV_SPLITS"], c["KV_CHUNK"]
+        if causal or c["PIPE"] == 2:
+            assert n == 1
+        if n == 1:
+            assert chunk == Skv
+            continue
+        # whole tiles, every split non-empty
+        assert chunk % c["BLOCK_N"] == 0
+        assert (n - 1) * chunk < Skv <= n * chunk
+        assert c["grid"] == B * H * c["n_qtiles"] * n
+    # every (tile, split count) pair appears once
+    keys = [(c["BLOCK_N"], c["WAVES"], c["PIPE"], c["KV_SPLITS"]) for c in cands]
+    assert len(keys) == len(set(keys))
+
+
+def test_key_splits_fill_the_device_only_when_it_is_underfilled():
+    desc = spec()
+    few = plan(desc, pa.KIND_FWD, 1, 2, 8192, 8192, 128)
+    assert few["KV_SPLITS"] > 1  # 2 heads x 32 q-tiles cannot fill 256 CUs
+    long_keys = plan(desc, pa.KIND_FWD, 1, 32, 256, 32768, 128)
+    assert long_keys["KV_SPLITS"] > 1
+    full = plan(desc, pa.KIND_FWD, 1, 32, 8192, 8192, 128)
+    assert full["KV_SPLITS"] == 1  # 1024 workgroups already fill it
+
+
+def test_key_split_model_charges_the_combine():
+    # with splits the model adds the partials' traffic and a second launch:
+    # on a shape that already fills the device a split can only cost time
+    desc = spec()
+    cands = pa.fwd_candidates(1, 32, 8192, 8192, 128, False, desc=desc)
+    by_tile = {}
+    for c in cands:
+        by_tile.setdefault((c["BLOCK_N"], c["WAVES"], c["PIPE"]), {})[c["KV_SPLITS"]] = c["modeled_us"]
+    for tile, times in by_tile.items():
+        if 2 in times:
+            assert times[2] > times[1] - 1e-9, tile
