@@ -19,6 +19,8 @@ What each function follows in the paper:
   * ``decode_split`` -- the Flash Decode decomposition in the HEG paragraph of
     the latency-modelling section (local softmax per chunk, gather partials,
     global softmax, final output).
+  * ``gemm`` -- the GEMM workload of the Evaluation section, C = A B, as its
+    plain definition.
 """
 from __future__ import annotations
 
@@ -87,9 +89,11 @@ class Oracle:
                                             f64p, f64p, f64p]
         lib.oracle_attn_gqa.argtypes = [u16p, u16p, u16p, f64p, f64p, ci, ci, ci, ci, ci, ci,
                                         cf, ci]
+        lib.oracle_gemm.argtypes = [u16p, u16p, f64p, f64p, ci, ci, ci, ci, i64p, ctypes.c_int64]
         lib.oracle_num_threads.argtypes = []
         for fn in (lib.oracle_attn, lib.oracle_attn_probs, lib.oracle_attn_rows,
-                   lib.oracle_decode_split, lib.oracle_num_threads, lib.oracle_attn_gqa):
+                   lib.oracle_decode_split, lib.oracle_num_threads, lib.oracle_attn_gqa,
+                   lib.oracle_gemm):
             fn.restype = ctypes.c_int
         self.lib = lib
         self.path = lib_path
@@ -178,6 +182,30 @@ class Oracle:
         return o
 
 
+    def gemm(self, a, b, M, N, K, b_nk=False, rows=None, with_abs=False):
+        """C = A B in fp64 ([M,N], or [len(rows),N] for a row subset); a is
+        [M,K], b is [K,N] or, with b_nk, [N,K].  With with_abs also returns
+        sum_k |a_mk b_kn| (the scale of any summation order's rounding)."""
+        a, b = _bits(a), _bits(b)
+        if a.size != M * K or b.size != K * N:
+            raise ValueError("oracle input sizes do not match the given dimensions")
+        null64 = ctypes.POINTER(ctypes.c_int64)()
+        nullf = ctypes.POINTER(ctypes.c_double)()
+        if rows is not None:
+            rows = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
+        n_out = M if rows is None else rows.size
+        c = np.empty((n_out, N), dtype=np.float64)
+        absc = np.empty((n_out, N), dtype=np.float64) if with_abs else None
+        rc = self.lib.oracle_gemm(_p(a, ctypes.c_uint16), _p(b, ctypes.c_uint16),
+                                  _p(c, ctypes.c_double),
+                                  _p(absc, ctypes.c_double) if with_abs else nullf, M, N, K,
+                                  int(bool(b_nk)),
+                                  _p(rows, ctypes.c_int64) if rows is not None else null64,
+                                  0 if rows is None else rows.size)
+        _check(rc, "gemm")
+        return (c, absc) if with_abs else c
+
+
 def default() -> Oracle:
     """The oracle built from oracle_attn.c (compiled on first use)."""
     global _default
@@ -208,3 +236,7 @@ def attn_rows(*a, **kw):
 
 def decode_split(*a, **kw):
     return default().decode_split(*a, **kw)
+
+
+def gemm(*a, **kw):
+    return default().gemm(*a, **kw)

@@ -303,3 +303,41 @@ int oracle_decode_split(const uint16_t* q, const uint16_t* k, const uint16_t* v,
     }
     return failed ? -4 : 0;
 }
+
+/*
+ * Matrix multiplication, the paper's third workload (Evaluation: GEMM, "a
+ * regular dense-linear-algebra primitive"), as its plain definition in fp64
+ * over bf16 inputs:
+ *     c[m][n] = sum_{k < K} a[m][k] * b(k, n)
+ * a: [M][K]; b: [K][N] with b(k, n) = b[k][n] (b_nk = 0), or [N][K] with
+ * b(k, n) = b[n][k] (b_nk = 1).  rows: NULL for every output row (c is
+ * [M][N]), else nrows row indices (c is [nrows][N]).  absc, if not NULL,
+ * receives sum_k |a[m][k] * b(k, n)| in the same layout (the scale of the
+ * rounding error of any summation order).  Products of two widened bf16
+ * values are exact in fp64; only the sum rounds.
+ */
+int oracle_gemm(const uint16_t* a, const uint16_t* b, double* c, double* absc, int M, int N,
+                int K, int b_nk, const int64_t* rows, int64_t nrows) {
+    if (M <= 0 || N <= 0 || K <= 0 || (b_nk != 0 && b_nk != 1)) return -1;
+    const int64_t n_out = rows ? nrows : (int64_t)M;
+    if (rows)
+        for (int64_t i = 0; i < nrows; ++i)
+            if (rows[i] < 0 || rows[i] >= M) return -1;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t i = 0; i < n_out; ++i) {
+        const int64_t m = rows ? rows[i] : i;
+        const uint16_t* arow = a + m * (int64_t)K;
+        for (int n = 0; n < N; ++n) {
+            double sum = 0.0, mag = 0.0;
+            for (int k = 0; k < K; ++k) {
+                const uint16_t bk = b_nk ? b[(int64_t)n * K + k] : b[(int64_t)k * N + n];
+                const double p = widen_bf16(arow[k]) * widen_bf16(bk);
+                sum += p;
+                mag += fabs(p);
+            }
+            c[i * N + n] = sum;
+            if (absc) absc[i * N + n] = mag;
+        }
+    }
+    return 0;
+}

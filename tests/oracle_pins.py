@@ -19,7 +19,12 @@ oracle disagrees with what mathematics or an independent library fixes:
 * grouped-query heads equal full heads with every key/value head repeated
   (and PyTorch's attention on them); the row log-sum-exp equals
   ``torch.logsumexp`` of independently computed scores, exp(s - lse) are the
-  probabilities, and Q = 0 or one key give closed forms.
+  probabilities, and Q = 0 or one key give closed forms;
+* GEMM: integer matrices give numpy's exact int64 product, tiny inputs the
+  exact rational sum, A I = A, ones A gives B's column sums, a rank-one
+  product its closed form, both B layouts agree and C^T = B^T A^T, numpy's
+  fp64 matmul agrees, row subsets are rows of the full product, and the
+  magnitude output is |A| |B|.
 
 ``tests/test_oracle.py`` runs every pin on the real oracle and on mutated
 copies of it (each with one planted mistake), and requires every mutant to
@@ -438,6 +443,102 @@ def pin_rejects_bad_args(orc):
             pass
         else:
             raise AssertionError("causal Sq > Skv accepted")
+
+
+# --------------------------------------------------------------------- GEMM
+def _int_bf16(shape, seed, lo=-8, hi=8):
+    """Small integers (exact in bf16; their products and sums are exact in fp64)."""
+    g = np.random.default_rng(seed)
+    vals = g.integers(lo, hi + 1, size=shape).astype(np.float32)
+    return from_float(torch.from_numpy(vals)), vals.astype(np.int64)
+
+
+def pin_gemm_integer_exact(orc):
+    # integer matrices: the exact product is numpy's int64 matmul
+    for (M, N, K), b_nk in (((7, 5, 9), False), ((16, 33, 130), True), ((1, 64, 1000), False)):
+        a, ai = _int_bf16((M, K), 3000 + K)
+        if b_nk:
+            b, bi = _int_bf16((N, K), 3001 + K)
+            want = ai @ bi.T
+        else:
+            b, bi = _int_bf16((K, N), 3001 + K)
+            want = ai @ bi
+        got = orc.gemm(a, b, M, N, K, b_nk=b_nk)
+        assert np.array_equal(got, want.astype(np.float64)), f"gemm integer {M, N, K, b_nk}"
+
+
+def pin_gemm_brute_force_fractions(orc):
+    # tiny random bf16 inputs, the exact rational sum, rounded once
+    from fractions import Fraction
+    M, N, K = 3, 4, 5
+    a, b = _rand((M, K), 3100), _rand((K, N), 3101)
+    af, bf = _f64(a).numpy(), _f64(b).numpy()
+    got = orc.gemm(a, b, M, N, K)
+    for m in range(M):
+        for n in range(N):
+            exact = sum(Fraction(float(af[m, k])) * Fraction(float(bf[k, n])) for k in range(K))
+            assert abs(got[m, n] - float(exact)) <= 4 * K * 2.0 ** -53 * abs(float(exact)) + 1e-300
+
+
+def pin_gemm_identity(orc):
+    M, K = 9, 12
+    a = _rand((M, K), 3200)
+    eye = from_float(torch.eye(K))
+    got = orc.gemm(a, eye, M, K, K)
+    assert np.array_equal(got, _f64(a).numpy()), "A I != A"
+    got_nk = orc.gemm(a, eye, M, K, K, b_nk=True)
+    assert np.array_equal(got_nk, _f64(a).numpy()), "A I != A (b as [N][K])"
+
+
+def pin_gemm_ones_column_sums(orc):
+    # A = ones: every output row is the column sums of B (exact fsum)
+    M, N, K = 4, 6, 50
+    a = from_float(torch.ones(M, K))
+    b = _rand((K, N), 3300)
+    bf = _f64(b).numpy()
+    got = orc.gemm(a, b, M, N, K)
+    sums = np.array([math.fsum(bf[:, n]) for n in range(N)])
+    _close(got, np.broadcast_to(sums, (M, N)), atol=1e-12, what="ones @ B")
+
+
+def pin_gemm_rank_one(orc):
+    # a[m][k] = x_m, b[k][n] = y_n (powers of two): c = K x_m y_n exactly
+    M, N, K = 5, 7, 24
+    x = 2.0 ** np.arange(-2, M - 2)
+    y = -(2.0 ** np.arange(-3, N - 3))
+    a = from_float(torch.from_numpy(np.repeat(x[:, None], K, 1).astype(np.float32)))
+    b = from_float(torch.from_numpy(np.repeat(y[None, :], K, 0).astype(np.float32)))
+    got = orc.gemm(a, b, M, N, K)
+    assert np.array_equal(got, K * np.outer(x, y)), "rank-one product"
+
+
+def pin_gemm_layouts_and_transpose(orc):
+    # B given as [N][K] equals B given as [K][N]; and C^T = B^T A^T
+    M, N, K = 11, 13, 40
+    a, b = _rand((M, K), 3400), _rand((K, N), 3401)
+    c = orc.gemm(a, b, M, N, K)
+    c_nk = orc.gemm(a, b.t().contiguous(), M, N, K, b_nk=True)
+    assert np.array_equal(c, c_nk), "b layouts disagree"
+    ct = orc.gemm(b.t().contiguous(), a.t().contiguous(), N, M, K)
+    _close(ct, c.T, atol=1e-12, what="transpose identity")
+
+
+def pin_gemm_numpy(orc):
+    M, N, K = 40, 24, 700
+    a, b = _rand((M, K), 3500), _rand((K, N), 3501)
+    want = _f64(a).numpy() @ _f64(b).numpy()
+    _close(orc.gemm(a, b, M, N, K), want, atol=1e-10, what="gemm vs numpy")
+
+
+def pin_gemm_rows_and_abs(orc):
+    M, N, K = 30, 8, 64
+    a, b = _rand((M, K), 3600), _rand((K, N), 3601)
+    full, absc = orc.gemm(a, b, M, N, K, with_abs=True)
+    rows = [29, 0, 17, 17]
+    assert np.array_equal(orc.gemm(a, b, M, N, K, rows=rows), full[rows]), "row subset"
+    want_abs = np.abs(_f64(a).numpy()) @ np.abs(_f64(b).numpy())
+    _close(absc, want_abs, atol=1e-10, what="sum of |products|")
+    assert np.all(absc >= np.abs(full) - 1e-12)
 
 
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

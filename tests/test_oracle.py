@@ -49,6 +49,16 @@ MUTANTS = [
      "const int64_t kvh = b * Hkv + h % Hkv;"),
     ("lse_without_stabiliser", "if (lse) *lse = m + log(l);", "if (lse) *lse = log(l);"),
     ("lse_base_two", "if (lse) *lse = m + log(l);", "if (lse) *lse = m + log2(l);"),
+    ("gemm_b_layouts_swapped", "b_nk ? b[(int64_t)n * K + k] : b[(int64_t)k * N + n]",
+     "b_nk ? b[(int64_t)k * N + n] : b[(int64_t)n * K + k]"),
+    ("gemm_drops_last_k", "for (int k = 0; k < K; ++k) {\n                const uint16_t bk",
+     "for (int k = 0; k < K - 1; ++k) {\n                const uint16_t bk"),
+    ("gemm_a_row_stride", "const uint16_t* arow = a + m * (int64_t)K;",
+     "const uint16_t* arow = a + m * (int64_t)N;"),
+    ("gemm_signed_magnitude", "mag += fabs(p);", "mag += p;"),
+    ("gemm_rows_ignored", "const int64_t m = rows ? rows[i] : i;", "const int64_t m = i;"),
+    ("gemm_first_k_skipped", "double sum = 0.0, mag = 0.0;\n            for (int k = 0;",
+     "double sum = 0.0, mag = 0.0;\n            for (int k = 1;"),
 ]
 
 
