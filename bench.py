@@ -1,6 +1,6 @@
 """Benchmark: tiled exact attention on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--no-gemm]
     python bench.py --config NAME      # one workload only (own JSON line)
 
 A step is one pass of the whole hot path over one batch of synthetic input:
@@ -13,8 +13,10 @@ runs on; the step wall time is bracketed by device synchronisation.
 Printed (one JSON line): value = prefill TFLOP/s (algorithmic flops: 4*d per
 unmasked (query, key) pair) with its MFMA roofline fraction; the decode leg's
 HBM GB/s (algorithmic bytes: K, V, Q read once, O written once) with its HBM
-roofline fraction; and the fp64 CPU oracle's rate on a bounded sample of the
-prefill workload, timed on this host's cores.
+roofline fraction; the fp64 CPU oracle's rate on a bounded sample of the
+prefill workload, timed on this host's cores; and, timed separately after the
+step, the GEMM workload (C = A B at M = N = K = 8192, bf16 in, fp32 out) with
+its MFMA roofline fraction.
 """
 from __future__ import annotations
 
@@ -74,6 +76,7 @@ def _args():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-gemm", action="store_true", help="skip the GEMM leg")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time for the oracle sample")
     ap.add_argument("--config", default=None, help="bench a single named workload")
@@ -238,9 +241,37 @@ def main():
                                 "kernel": "decode_partial_kernel + split_combine_kernel",
                                 "bytes_per_call": wd.hbm_bytes()}},
     }
+    if not a.no_gemm:
+        rec["gemm"] = gemm_leg(pa, dev)
     if not a.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(wp, qp, kp, vp, a.cpu_seconds)
     print(json.dumps(rec), flush=True)
+
+
+def gemm_leg(pa, dev, M=8192, N=8192, K=8192, steps=20, warmup=10) -> dict:
+    """The GEMM workload (C = A B, bf16 in, fp32 out) timed on its own after
+    the attention step, outside its timed region."""
+    import torch
+    from attn_inputs import random_bf16
+    a = random_bf16((M, K), 31).to(dev)
+    b = random_bf16((K, N), 32).to(dev)
+    c = torch.empty((M, N), dtype=torch.float32, device=dev)
+    for _ in range(warmup):
+        pa.gemm(a, b, c)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        pa.gemm(a, b, c)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    tflops = 2.0 * M * N * K / (ms * 1e-3) / 1e12
+    return {"M": M, "N": N, "K": K, "value": tflops, "unit": "TFLOP/s", "ms_per_call": ms,
+            "plan": pa.gemm_plan(M, N, K),
+            "roofline": {"bound": "mfma", "achieved": tflops, "peak": PEAK_BF16_TFLOPS,
+                         "unit": "TFLOP/s", "frac": tflops / PEAK_BF16_TFLOPS,
+                         "kernel": "gemm_kernel"}}
 
 
 if __name__ == "__main__":

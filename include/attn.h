@@ -49,8 +49,10 @@ extern "C" {
 #define ATTN_KIND_FWD 0
 #define ATTN_KIND_DECODE 1
 
-/* attn_fwd_ex flags */
-#define ATTN_OUT_BF16 1        /* o is bf16 (round to nearest even) instead of fp32 */
+/* attn_fwd_ex and attn_gemm flags */
+#define ATTN_OUT_BF16 1        /* the output is bf16 (round to nearest even) instead of fp32 */
+/* attn_gemm flag */
+#define ATTN_GEMM_B_NK 2       /* B is stored [N][K] (B^T row-major) instead of [K][N] */
 
 /*
  * Prefill attention (Flash Attention).
@@ -210,6 +212,34 @@ int attn_get_plan(int kind, int B, int H, int Sq, int Skv, int d, int causal, in
                   char* buf, int buflen);
 int attn_get_plan_for(const attn_device_desc* desc, int kind, int B, int H, int Sq, int Skv,
                       int d, int causal, int n_splits, char* buf, int buflen);
+
+/*
+ * Matrix multiplication C = A B, the paper's GEMM workload (Evaluation,
+ * GEMM: "a regular dense-linear-algebra primitive with structured tiling
+ * and high data reuse"), tiled by the same latency model.
+ *   a: bf16 [M][K] row-major.
+ *   b: bf16 [K][N] row-major, or with ATTN_GEMM_B_NK bf16 [N][K] row-major
+ *      (c[m][n] = sum_k a[m][k] * b[n][k]).
+ *   c: [M][N] row-major, fp32, or bf16 with ATTN_OUT_BF16 (caller-allocated,
+ *      fully overwritten).
+ * Work: bf16 MFMA products with fp32 accumulation (blocked summation order),
+ * rounded once to the output type.  Supported: M >= 1, N and K multiples of
+ * 8 (16-byte rows), A and B each at most 2 GiB.  Asynchronous on the
+ * thread's stream; allocates nothing.
+ * Errors: EINVAL for null or misaligned pointers, dims <= 0 or unknown
+ * flags; EUNSUPPORTED for N or K not a multiple of 8, operands over 2 GiB,
+ * or a device that is not gfx950; EHIP for launch errors.
+ */
+int attn_gemm(const void* a, const void* b, void* c, int M, int N, int K, int flags);
+
+/* GEMM plan query (host only): the named tile symbols BLOCK_M, BLOCK_N,
+ * BLOCK_K, WAVES_M, WAVES_N, PIPE, the grid, the modelled time in us and the
+ * binding resource, as one NUL-terminated line in buf (truncated to buflen).
+ * desc NULL: this device's description and its compiled kernels' real
+ * register/occupancy footprint.  Returns the full line length or a
+ * negative ATTN_E* code (the same argument checks as attn_gemm). */
+int attn_gemm_plan(const attn_device_desc* desc, int M, int N, int K, int flags, char* buf,
+                   int buflen);
 
 #ifdef __cplusplus
 }

@@ -27,12 +27,13 @@ ATTN_ENOMEM = -4
 KIND_FWD = 0
 KIND_DECODE = 1
 ATTN_OUT_BF16 = 1
+ATTN_GEMM_B_NK = 2
 
 # Entry points declared in include/attn.h.
 EXPORTED = ("attn_fwd", "attn_decode", "attn_fwd_ex", "attn_decode_ex",
             "attn_decode_workspace_bytes", "attn_set_stream", "attn_get_stream",
             "attn_last_error", "attn_query_device", "attn_measure_device", "attn_get_plan",
-            "attn_get_plan_for")
+            "attn_get_plan_for", "attn_gemm", "attn_gemm_plan")
 
 
 class AttnError(RuntimeError):
@@ -105,10 +106,16 @@ def _load() -> ctypes.CDLL:
                                       ci, ctypes.c_char_p, ci]
     lib.attn__fwd_candidates.argtypes = [ctypes.POINTER(DeviceDesc), ci, ci, ci, ci, ci, ci, ci,
                                          ctypes.c_char_p, ci]
+    lib.attn_gemm.argtypes = [vp, vp, vp, ci, ci, ci, ci]
+    lib.attn_gemm_plan.argtypes = [ctypes.POINTER(DeviceDesc), ci, ci, ci, ci, ctypes.c_char_p,
+                                   ci]
+    lib.attn__gemm_candidates.argtypes = [ctypes.POINTER(DeviceDesc), ci, ci, ci, ci, ci,
+                                          ctypes.c_char_p, ci]
     for fn in (lib.attn_fwd, lib.attn_decode, lib.attn_fwd_ex, lib.attn_decode_ex,
                lib.attn_set_stream, lib.attn_query_device,
                lib.attn_measure_device, lib.attn_get_plan, lib.attn_get_plan_for,
-               lib.attn__fwd_candidates):
+               lib.attn__fwd_candidates, lib.attn_gemm, lib.attn_gemm_plan,
+               lib.attn__gemm_candidates):
         fn.restype = ci
     return lib
 
@@ -207,6 +214,50 @@ def decode_workspace_bytes(B: int, Hq: int, Hkv: int, Skv: int, d: int, n_splits
     if n < 0:
         raise AttnError(int(n), last_error())
     return int(n)
+
+
+def gemm(a, b, c=None, b_nk: bool = False, out_dtype=None):
+    """C = A B on bf16 MFMA with fp32 accumulation.  a: bf16 [M,K]; b: bf16
+    [K,N], or [N,K] with b_nk; returns c [M,N] fp32 (or out_dtype bf16)."""
+    import torch
+    M, K = a.shape
+    N = b.shape[0] if b_nk else b.shape[1]
+    _require(a, torch.bfloat16, (M, K), "a")
+    _require(b, torch.bfloat16, (N, K) if b_nk else (K, N), "b")
+    if out_dtype is None:
+        out_dtype = c.dtype if c is not None else torch.float32
+    if out_dtype not in (torch.float32, torch.bfloat16):
+        raise ValueError("out_dtype must be torch.float32 or torch.bfloat16")
+    if c is None:
+        c = torch.empty((M, N), dtype=out_dtype, device=a.device)
+    _require(c, out_dtype, (M, N), "c")
+    flags = (ATTN_OUT_BF16 if out_dtype == torch.bfloat16 else 0) | \
+        (ATTN_GEMM_B_NK if b_nk else 0)
+    _set_stream(a)
+    _check(lib.attn_gemm(a.data_ptr(), b.data_ptr(), c.data_ptr(), M, N, K, flags))
+    return c
+
+
+def gemm_plan(M: int, N: int, K: int, b_nk: bool = False, desc: DeviceDesc | None = None) -> str:
+    buf = ctypes.create_string_buffer(512)
+    ptr = ctypes.byref(desc) if desc is not None else None
+    rc = lib.attn_gemm_plan(ptr, M, N, K, ATTN_GEMM_B_NK if b_nk else 0, buf, 512)
+    if rc < 0:
+        raise AttnError(rc, last_error())
+    return buf.value.decode()
+
+
+def gemm_candidates(M: int, N: int, K: int, b_nk: bool = False, desc: DeviceDesc | None = None,
+                    device_footprint: bool = False) -> list[dict]:
+    """Every feasible GEMM candidate with its modelled time (not ABI; for the
+    block-size ablation)."""
+    buf = ctypes.create_string_buffer(1 << 16)
+    ptr = ctypes.byref(desc) if desc is not None else None
+    rc = lib.attn__gemm_candidates(ptr, M, N, K, ATTN_GEMM_B_NK if b_nk else 0,
+                                   int(bool(device_footprint)), buf, 1 << 16)
+    if rc < 0:
+        raise AttnError(rc, last_error())
+    return [parse_plan(l) for l in buf.value.decode().splitlines() if l.strip()]
 
 
 def query_device() -> dict:

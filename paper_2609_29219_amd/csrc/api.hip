@@ -121,6 +121,7 @@ std::mutex g_mu;
 std::map<int, DeviceState> g_devices;
 std::map<std::tuple<int, int, int, int, int, int, int, int>, FwdPlan> g_fwd_cache;
 std::map<std::tuple<int, int, int, int, int, int, int>, DecodePlan> g_dec_cache;
+std::map<std::tuple<int, int, int, int, int>, GemmPlan> g_gemm_cache;
 
 // Structural properties from the runtime; performance properties from the
 // built-in gfx950 description.
@@ -196,6 +197,22 @@ int stream_workspace(DeviceState* st, size_t bytes, void** out) {
     }
     *out = w.ptr;
     return ATTN_OK;
+}
+
+// Optional fixed GEMM tile for the block-size ablation only:
+// ATTN_FORCE_GEMM="bm=256,bn=256,bk=64,wm=2,wn=4,pipe=1".  Never used to
+// select tiles.
+bool forced_gemm(int* bm, int* bn, int* bk, int* wm, int* wn, int* pipe) {
+    const char* s = getenv("ATTN_FORCE_GEMM");
+    if (!s || !*s) return false;
+    return sscanf(s, "bm=%d,bn=%d,bk=%d,wm=%d,wn=%d,pipe=%d", bm, bn, bk, wm, wn, pipe) == 6;
+}
+
+// Forced tiles (ablation only) may run a variant that spills: slow, not wrong.
+bool gemm_resources_forced(const GemmPlan& p, KernelRes* r) {
+    if (!gemm_resources(p, r)) return false;
+    r->scratch_bytes = 0;
+    return true;
 }
 
 int validate_common(const void* q, const void* k, const void* v, const void* o, int B, int H,
@@ -454,6 +471,101 @@ int attn_decode_ex(const void* q, const void* k, const void* v, float* o, float*
 int attn_decode(const void* q, const void* k, const void* v, float* o, int B, int H, int Skv,
                 int d, int n_splits) {
     return attn_decode_ex(q, k, v, o, nullptr, B, H, H, Skv, d, n_splits, nullptr, 0);
+}
+
+// ---------------------------------------------------------------- GEMM --
+static int validate_gemm_dims(int M, int N, int K, int flags) {
+    if (M <= 0 || N <= 0 || K <= 0)
+        return fail(ATTN_EINVAL, "dimensions must be positive (M=%d N=%d K=%d)", M, N, K);
+    if (flags & ~(ATTN_OUT_BF16 | ATTN_GEMM_B_NK))
+        return fail(ATTN_EINVAL, "unknown flags 0x%x", flags);
+    if (K % 8 != 0 || N % 8 != 0)
+        return fail(ATTN_EUNSUPPORTED, "K (%d) and N (%d) must be multiples of 8", K, N);
+    if ((long long)M * K * 2 > 0x7fffffffLL || (long long)N * K * 2 > 0x7fffffffLL)
+        return fail(ATTN_EUNSUPPORTED, "A or B exceeds 2 GiB");
+    return ATTN_OK;
+}
+
+int attn_gemm_plan(const attn_device_desc* desc, int M, int N, int K, int flags, char* buf,
+                   int buflen) {
+    attn_device_desc local;
+    GemmResFn res = nullptr;
+    if (!desc) {
+        const int q = attn_query_device(&local);
+        if (q == ATTN_OK && strcmp(local.arch, "gfx950") == 0) res = gemm_resources;
+        desc = &local;
+    }
+    if (buflen < 0 || (buflen > 0 && !buf)) return fail(ATTN_EINVAL, "bad output buffer");
+    int rc = validate_gemm_dims(M, N, K, flags);
+    if (rc) return rc;
+    GemmPlan p;
+    if (!plan_gemm(*desc, M, N, K, (flags & ATTN_GEMM_B_NK) ? 1 : 0, &p, res))
+        return fail(ATTN_EUNSUPPORTED, "no feasible GEMM plan");
+    return format_gemm_plan(p, buf, buflen);
+}
+
+// Not part of the ABI: every feasible GEMM candidate with its modelled time,
+// one plan line each (for the block-size ablation).  Returns the full length.
+int attn__gemm_candidates(const attn_device_desc* desc, int M, int N, int K, int flags,
+                          int device_footprint, char* buf, int buflen) {
+    attn_device_desc local;
+    GemmResFn res = nullptr;
+    const bool have = attn_query_device(&local) == ATTN_OK && strcmp(local.arch, "gfx950") == 0;
+    if (have && (device_footprint || !desc)) res = gemm_resources;
+    if (!desc) desc = &local;
+    if (buflen < 0 || (buflen > 0 && !buf)) return fail(ATTN_EINVAL, "bad output buffer");
+    int rc = validate_gemm_dims(M, N, K, flags);
+    if (rc) return rc;
+    GemmPlan plans[64];
+    const int n = std::min(64, plan_gemm_all(*desc, M, N, K, (flags & ATTN_GEMM_B_NK) ? 1 : 0,
+                                             plans, 64, res));
+    int len = 0;
+    for (int i = 0; i < n; ++i) {
+        char line[512];
+        const int l = format_gemm_plan(plans[i], line, sizeof line);
+        if (buf && len + l + 1 < buflen) {
+            memcpy(buf + len, line, l);
+            buf[len + l] = '\n';
+            buf[len + l + 1] = '\0';
+        }
+        len += l + 1;
+    }
+    if (buf && buflen > 0 && len >= buflen) buf[buflen - 1] = '\0';
+    return len;
+}
+
+int attn_gemm(const void* a, const void* b, void* c, int M, int N, int K, int flags) {
+    if (!a || !b || !c) return fail(ATTN_EINVAL, "null matrix pointer");
+    if (!aligned16(a) || !aligned16(b) || !aligned16(c))
+        return fail(ATTN_EINVAL, "matrix pointers must be 16-byte aligned");
+    int rc = validate_gemm_dims(M, N, K, flags);
+    if (rc) return rc;
+    DeviceState* st = nullptr;
+    rc = device_state(&st);
+    if (rc) return rc;
+    const int b_nk = (flags & ATTN_GEMM_B_NK) ? 1 : 0;
+    GemmPlan plan;
+    int bm, bn, bk, wm, wn, pipe;
+    if (forced_gemm(&bm, &bn, &bk, &wm, &wn, &pipe)) {
+        if (!plan_gemm_fixed(st->desc, M, N, K, b_nk, bm, bn, bk, wm, wn, pipe, &plan,
+                             gemm_resources_forced))
+            return fail(ATTN_EINVAL, "ATTN_FORCE_GEMM names an infeasible or unknown tile");
+    } else {
+        std::lock_guard<std::mutex> lk(g_mu);
+        auto key = std::make_tuple(M, N, K, b_nk, st->desc.num_cus);
+        auto it = g_gemm_cache.find(key);
+        if (it != g_gemm_cache.end()) {
+            plan = it->second;
+        } else {
+            if (!plan_gemm(st->desc, M, N, K, b_nk, &plan, gemm_resources))
+                return fail(ATTN_EUNSUPPORTED, "no feasible GEMM plan for this shape");
+            g_gemm_cache[key] = plan;
+        }
+    }
+    const hipError_t e = launch_gemm(plan, a, b, c, M, N, K, (flags & ATTN_OUT_BF16) ? 1 : 0,
+                                     st->desc.num_xcds, t_stream);
+    if (e != hipSuccess) return fail_hip(e, "GEMM launch");
+    return ATTN_OK;
 }
 
 }  // extern "C"

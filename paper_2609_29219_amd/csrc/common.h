@@ -43,6 +43,33 @@ struct DecodePlan {
     const char* bound = "";
 };
 
+// Symbols of the GEMM kernel (C = A B, bf16 in, fp32 accumulation).
+struct GemmPlan {
+    int block_m = 0, block_n = 0, block_k = 0;  // workgroup tile of C and k-step
+    int waves_m = 0, waves_n = 0;               // wave grid inside the tile
+    int pipe = 0;        // LDS slots - 1: k-tiles in flight while one is multiplied
+    int b_nk = 0;        // B stored [N][K] (else [K][N])
+    int lds_bytes = 0;
+    int vgprs = 0;
+    int wg_per_cu = 0;
+    int tiles_m = 0, tiles_n = 0;
+    long long grid = 0;
+    double modeled_us = 0.0;
+    const char* bound = "";
+};
+
+// Arguments of one GEMM launch.
+struct GemmArgs {
+    const uint16_t* a;  // bf16 [M][K]
+    const uint16_t* b;  // bf16 [K][N] or [N][K]
+    void* c;            // [M][N] fp32 or bf16 (out_bf16)
+    int M, N, K;
+    int tiles_m, tiles_n;
+    int n_wg;
+    int num_xcds;
+    int out_bf16;
+};
+
 // Candidate domains: every point is an instantiated kernel.
 constexpr int kFwdBlockN[] = {32, 64, 128};
 constexpr int kFwdWaves[] = {4, 8};
@@ -116,6 +143,18 @@ int plan_fwd_all(const attn_device_desc& desc, int B, int H, int Sq, int Skv, in
 bool fwd_resources(int d, int bn, int waves, int pipe, int causal, KernelRes* out);
 bool plan_decode(const attn_device_desc& desc, int B, int Hq, int Hkv, int Skv, int d,
                  int n_splits, DecodePlan* out);
+// GEMM planner: the same latency model (HEG pipe and for nodes over the
+// device description); res, when given, supplies the compiled kernels' real
+// footprint.
+typedef bool (*GemmResFn)(const GemmPlan& p, KernelRes* out);
+bool plan_gemm_fixed(const attn_device_desc& desc, int M, int N, int K, int b_nk, int bm, int bn,
+                     int bk, int wm, int wn, int pipe, GemmPlan* out, GemmResFn res = nullptr);
+bool plan_gemm(const attn_device_desc& desc, int M, int N, int K, int b_nk, GemmPlan* out,
+               GemmResFn res = nullptr);
+int plan_gemm_all(const attn_device_desc& desc, int M, int N, int K, int b_nk, GemmPlan* out,
+                  int cap, GemmResFn res = nullptr);
+bool gemm_resources(const GemmPlan& p, KernelRes* out);
+int format_gemm_plan(const GemmPlan& p, char* buf, int buflen);
 int format_fwd_plan(const FwdPlan& p, char* buf, int buflen);
 int format_decode_plan(const DecodePlan& p, char* buf, int buflen);
 
@@ -135,6 +174,8 @@ hipError_t launch_split_combine(int d, const float* ws_m, const float* ws_l, con
 hipError_t launch_decode(const DecodePlan& p, const void* q, const void* k, const void* v,
                          float* o, float* lse, float* workspace, int B, int Hq, int Hkv, int Skv,
                          float scale, hipStream_t stream);
+hipError_t launch_gemm(const GemmPlan& p, const void* a, const void* b, void* c, int M, int N,
+                       int K, int out_bf16, int num_xcds, hipStream_t stream);
 // Query heads of one key/value group that a decode workgroup serves together.
 int decode_heads_per_wg(int group);
 

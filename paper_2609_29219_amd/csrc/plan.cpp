@@ -280,6 +280,180 @@ int plan_fwd_all(const attn_device_desc& desc, int B, int H, int Sq, int Skv, in
     return n;
 }
 
+// ------------------------------------------------------------------ GEMM --
+// Compiled GEMM tiles (BM, BN, BK, wave grid WM x WN); each exists for both B
+// layouts and for every pipe setting (1, 2 or 3 LDS slots) whose LDS fits.
+struct GemmTile {
+    int bm, bn, bk, wm, wn;
+};
+static constexpr int kGemmGroupM = 8;  // tile rows per group of the workgroup order
+static constexpr GemmTile kGemmTiles[] = {
+    {64, 64, 64, 2, 2},    {128, 128, 32, 2, 2}, {128, 128, 64, 2, 2},
+    {256, 128, 32, 2, 2},  {256, 128, 64, 2, 2}, {128, 256, 32, 2, 2},
+    {128, 256, 64, 2, 2},  {256, 256, 32, 2, 4}, {256, 256, 64, 2, 4},
+};
+
+int gemm_lds_bytes(int bm, int bn, int bk, int b_nk, int pipe) {
+    const int a = bm * (bk + 8);
+    const int b = b_nk ? bn * (bk + 8) : bk * (bn + 32);
+    return (pipe + 1) * (a + b) * 2;
+}
+
+// The GEMM as an HEG (the paper's GEMM workload with the same latency model
+// as the prefill):
+//   for(k-tiles, pipe(load, body, -)) per workgroup; workgroups in rounds of
+//   (CUs x resident workgroups per CU, g).
+// body of one k-tile of one workgroup: the larger of
+//   MFMA: 2*BM*BN*BK / mfma_flops_per_clk_cu
+//   LDS:  (waves * (MB + NB) * 64 B per k + (BM + BN) * BK * 2) / lds_bytes_per_clk
+// g workgroups share the CU: a round (each of them advancing one k-tile)
+// takes at least g bodies plus a barrier (tile_sync_cycles).  The load of a
+// k-tile takes the latency of where its bytes come from: the tiles resident
+// on one XCD share A row panels and B column panels in its L2 (GM tile rows
+// per group of the workgroup order), so only the share of the bytes that
+// one XCD's resident tiles need once comes from HBM (hbm_latency_us), the
+// rest from L2 (tile_latency_cycles).  Pipe knob (Eq. heg-pipe, load/body
+// boundary): with pipe 0 the load is exposed, a round takes load + body (or
+// g bodies, if longer); with pipe p >= 1, p k-tiles are in flight and a
+// round takes the larger of load / p and g bodies.  The HBM bytes of a round
+// bound it from below at this CU's share of the HBM bandwidth.  Each
+// workgroup adds one exposed load (its first k-tile) and its C store.  This
+// is the double-buffering against tile-size trade-off: each extra slot adds
+// a tile of LDS, which can cost resident workgroups or rule the largest
+// tiles out.  Lower bounds over the whole product: HBM (A, B read once, C
+// written once) and L2 (A re-read once per tile column, B once per tile row).
+bool plan_gemm_fixed(const attn_device_desc& desc, int M, int N, int K, int b_nk, int bm, int bn,
+                     int bk, int wm, int wn, int pipe, GemmPlan* out, GemmResFn res) {
+    bool known = false;
+    for (const GemmTile& t : kGemmTiles)
+        known |= t.bm == bm && t.bn == bn && t.bk == bk && t.wm == wm && t.wn == wn;
+    if (!known || pipe < 0 || pipe > 2) return false;
+    GemmPlan p;
+    p.block_m = bm;
+    p.block_n = bn;
+    p.block_k = bk;
+    p.waves_m = wm;
+    p.waves_n = wn;
+    p.pipe = pipe;
+    p.b_nk = b_nk ? 1 : 0;
+    p.lds_bytes = gemm_lds_bytes(bm, bn, bk, b_nk, pipe);
+    const int waves = wm * wn;
+    const int mb = bm / (32 * wm), nb = bn / (32 * wn);
+    p.vgprs = mb * nb * 16 + 48 + 8 * (mb + nb);  // accumulators, operands, addresses
+    if (p.lds_bytes > desc.lds_bytes_per_cu) return false;
+    const int simds = desc.simds_per_cu;
+    const int wpe_regs = desc.vgprs_per_simd_lane / std::max(p.vgprs, 1);
+    int g = desc.lds_bytes_per_cu / p.lds_bytes;
+    g = std::min(g, (wpe_regs * simds) / waves);
+    g = std::min(g, (desc.max_waves_per_simd * simds) / waves);
+    if (res) {
+        KernelRes kr;
+        if (!res(p, &kr)) return false;
+        if (kr.scratch_bytes > 0) return false;  // spills: not a valid primitive
+        g = kr.wg_per_cu;
+        if (kr.vgprs > 0) p.vgprs = kr.vgprs;
+    }
+    if (g < 1) return false;
+    p.tiles_m = (M + bm - 1) / bm;
+    p.tiles_n = (N + bn - 1) / bn;
+    p.grid = (long long)p.tiles_m * p.tiles_n;
+    if (p.grid > 0x7fffffffLL) return false;
+    p.wg_per_cu = g;
+    // resident workgroups per CU: no more than the grid gives each CU
+    const double gr = std::min<double>(g, ceil((double)p.grid / desc.num_cus));
+
+    // ---- one k-tile --------------------------------------------------------
+    const double compute = 2.0 * bm * bn * bk / desc.mfma_bf16_flops_per_clk_cu;
+    const double lds_bytes = waves * (double)(mb + nb) * 64.0 * bk + (double)(bm + bn) * bk * 2.0;
+    const double lds = lds_bytes / desc.lds_bytes_per_clk_cu;
+    const double body1 = std::max(compute, lds);
+    const double body_g = gr * body1 + desc.tile_sync_cycles;
+    // HBM share of a k-tile's bytes: the resident tiles of one XCD need each
+    // of their distinct A and B panels once
+    const double a_bytes = (double)bm * bk * 2.0, b_bytes = (double)bn * bk * 2.0;
+    const double cus_xcd = (double)desc.num_cus / desc.num_xcds;
+    const double xcd_tiles = std::max(1.0, std::min((double)p.grid / desc.num_xcds, cus_xcd * gr));
+    const double dm = std::min({(double)kGemmGroupM, (double)p.tiles_m, xcd_tiles});
+    const double dn = std::max(1.0, std::min((double)p.tiles_n, xcd_tiles / dm));
+    const double hbm_per_wg = std::min(a_bytes + b_bytes, (dm * a_bytes + dn * b_bytes) / xcd_tiles);
+    const double f_hbm = hbm_per_wg / (a_bytes + b_bytes);
+    const double hbm_lat = desc.hbm_latency_us * desc.clock_ghz * 1e3;  // cycles
+    const double load = (1.0 - f_hbm) * desc.tile_latency_cycles + f_hbm * hbm_lat;
+    const double cu_bw = desc.hbm_bytes_per_s / desc.num_cus / (desc.clock_ghz * 1e9);  // B/clk
+    const double t_bw = gr * hbm_per_wg / cu_bw;
+    double round = pipe == 0 ? std::max(heg_pipe(load, body1, 0.0, 0, 0), body_g)
+                             : heg_pipe(load / pipe, body_g, 0.0, 1, 0);
+    round = std::max(round, t_bw);
+
+    const int n_k = (K + bk - 1) / bk;
+    const double store = gr * (double)bm * bn * 4.0 / cu_bw;
+    const double rounds = ceil((double)p.grid / (desc.num_cus * gr));
+    const double cycles = rounds * (load + heg_for(n_k, round) + store);
+    double us = cycles / (desc.clock_ghz * 1e3);
+    const double hbm_us =
+        ((double)M * K * 2.0 + (double)K * N * 2.0 + (double)M * N * 4.0) / desc.hbm_bytes_per_s *
+        1e6;
+    const double l2_bytes = (double)M * K * 2.0 * p.tiles_n + (double)K * N * 2.0 * p.tiles_m;
+    const double l2_us =
+        l2_bytes / (desc.l2_bytes_per_clk_xcd * desc.num_xcds * desc.clock_ghz * 1e9) * 1e6;
+    const char* bound = lds > compute ? "lds" : "mfma";
+    if (round > body_g) bound = t_bw >= round ? "hbm" : "latency";
+    if (hbm_us > us) {
+        us = hbm_us;
+        bound = "hbm";
+    }
+    if (l2_us > us) {
+        us = l2_us;
+        bound = "l2";
+    }
+    p.modeled_us = us + desc.launch_us;
+    p.bound = bound;
+    *out = p;
+    return true;
+}
+
+int plan_gemm_all(const attn_device_desc& desc, int M, int N, int K, int b_nk, GemmPlan* out,
+                  int cap, GemmResFn res) {
+    int n = 0;
+    for (const GemmTile& t : kGemmTiles)
+        for (int pipe : {0, 1, 2}) {
+            GemmPlan p;
+            if (!plan_gemm_fixed(desc, M, N, K, b_nk, t.bm, t.bn, t.bk, t.wm, t.wn, pipe, &p, res))
+                continue;
+            if (n < cap) out[n] = p;
+            ++n;
+        }
+    return n;
+}
+
+bool plan_gemm(const attn_device_desc& desc, int M, int N, int K, int b_nk, GemmPlan* out,
+               GemmResFn res) {
+    bool found = false;
+    GemmPlan best;
+    for (const GemmTile& t : kGemmTiles)
+        for (int pipe : {0, 1, 2}) {
+            GemmPlan p;
+            if (!plan_gemm_fixed(desc, M, N, K, b_nk, t.bm, t.bn, t.bk, t.wm, t.wn, pipe, &p, res))
+                continue;
+            if (!found || p.modeled_us < best.modeled_us * (1.0 - 1e-9)) {
+                best = p;
+                found = true;
+            }
+        }
+    if (found) *out = best;
+    return found;
+}
+
+int format_gemm_plan(const GemmPlan& p, char* buf, int buflen) {
+    return snprintf(buf, buf ? (size_t)buflen : 0,
+                    "kind=gemm BLOCK_M=%d BLOCK_N=%d BLOCK_K=%d WAVES_M=%d WAVES_N=%d PIPE=%d "
+                    "b_nk=%d grid=%lld tiles_m=%d tiles_n=%d lds_bytes=%d vgprs=%d wg_per_cu=%d "
+                    "modeled_us=%.3f bound=%s",
+                    p.block_m, p.block_n, p.block_k, p.waves_m, p.waves_n, p.pipe, p.b_nk, p.grid,
+                    p.tiles_m, p.tiles_n, p.lds_bytes, p.vgprs, p.wg_per_cu, p.modeled_us,
+                    p.bound);
+}
+
 // Query heads per decode workgroup: the largest of 8, 4, 2, 1 dividing the
 // number of query heads that share a key/value head.
 int decode_heads_per_wg(int group) {

@@ -1,7 +1,7 @@
 """Planner validation on the device: the block-size ablation.
 
     python paper_2609_29219_amd/plan_ablation.py [--save FILE] [--load FILE] [--fit]
-                                                 [--markdown FILE]
+                                                 [--markdown FILE] [--gemm]
 
 For each workload every feasible prefill candidate (block sizes, waves,
 pipeline knob, key splits) is run through the ATTN_FORCE_PLAN hook and timed, and set
@@ -13,6 +13,12 @@ step up or down, the other wave count, the neighbouring pipeline knob, the
 neighbouring key-split count).  The
 paper validates its model the same way (top-k candidates and block-size
 neighbourhoods); measurement here validates, it never selects.
+
+--gemm runs the same validation for the GEMM over the paper's shape range
+(256 to 16384, square and skewed): every feasible tile (BM, BN, BK, wave
+grid, pipe) is timed; the report gives the planner pick's measured and
+modelled TFLOP/s, its rank, and its rank among the tiles one legal step away
+in BM, BN, BK and pipe (the paper's local block-size perturbation).
 
 --fit refits the four offline-calibrated fields of the device description
 (issue_cycles_per_score, valu_mfma_overlap, tile_sync_cycles,
@@ -186,17 +192,139 @@ def markdown(summaries: list, fitted: dict | None) -> str:
     return "\n".join(out)
 
 
+# ------------------------------------------------------------------ GEMM --
+# (M, N, K): squares across the paper's range and its skewed shapes
+GEMM_SHAPES = [(256, 256, 256), (1024, 1024, 1024), (2048, 2048, 2048), (4096, 4096, 4096),
+               (8192, 8192, 8192), (16384, 16384, 16384), (16384, 256, 2048), (256, 256, 2048),
+               (16384, 256, 16384), (2048, 2048, 16384)]
+GEMM_DOMAINS = ((64, 128, 256), (64, 128, 256), (32, 64), (0, 1, 2))  # BM, BN, BK, pipe
+
+
+def gemm_key(c: dict) -> tuple:
+    return (c["BLOCK_M"], c["BLOCK_N"], c["BLOCK_K"], c["WAVES_M"], c["WAVES_N"], c["PIPE"])
+
+
+def time_gemm(shape, variant, reps=3) -> float:
+    """Best-of-reps mean time (us) of back-to-back launches of one forced tile."""
+    import torch
+    from attn_inputs import random_bf16
+    M, N, K = shape
+    if not hasattr(time_gemm, "cache") or time_gemm.cache[0] != shape:
+        a = random_bf16((M, K), 21).cuda()
+        b = random_bf16((K, N), 22).cuda()
+        c = torch.empty((M, N), dtype=torch.float32, device="cuda")
+        time_gemm.cache = (shape, a, b, c)
+    _, a, b, c = time_gemm.cache
+    iters = 3 if M * N * K > 2 ** 40 else 10
+    os.environ["ATTN_FORCE_GEMM"] = "bm=%d,bn=%d,bk=%d,wm=%d,wn=%d,pipe=%d" % variant
+    try:
+        for _ in range(3):
+            pa.gemm(a, b, c)
+        torch.cuda.synchronize()
+        best = float("inf")
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(iters):
+                pa.gemm(a, b, c)
+            e1.record()
+            torch.cuda.synchronize()
+            best = min(best, e0.elapsed_time(e1) / iters * 1e3)
+        return best
+    finally:
+        os.environ.pop("ATTN_FORCE_GEMM", None)
+
+
+def gemm_neighbours(pick: tuple, feasible: set) -> list:
+    """Feasible tiles whose BM, BN, BK and pipe are each at most one legal
+    step from the pick's (the paper's local block-size perturbation)."""
+    out = []
+    for c in feasible:
+        steps = [abs(dom.index(x) - dom.index(y))
+                 for dom, x, y in zip(GEMM_DOMAINS, (c[0], c[1], c[2], c[5]),
+                                      (pick[0], pick[1], pick[2], pick[5]))]
+        if max(steps) <= 1 and c != pick:
+            out.append(c)
+    return sorted(out)
+
+
+def gemm_summary(shape, cands: list, meas: dict) -> dict:
+    M, N, K = shape
+    flops = 2.0 * M * N * K
+    rows = [(c["modeled_us"], meas[gemm_key(c)], gemm_key(c)) for c in cands
+            if gemm_key(c) in meas]
+    by_model = sorted(rows)
+    by_meas = sorted(rows, key=lambda r: r[1])
+    pick, best = by_model[0], by_meas[0]
+    nb = gemm_neighbours(pick[2], {r[2] for r in rows})
+    return {
+        "shape": shape, "candidates": len(rows), "pick": pick[2], "pick_us": pick[1],
+        "pick_tflops": flops / pick[1] / 1e6, "pick_modeled_tflops": flops / pick[0] / 1e6,
+        "best": best[2], "best_us": best[1], "pick_over_best": pick[1] / best[1] - 1.0,
+        "pick_measured_rank": [r[2] for r in by_meas].index(pick[2]) + 1,
+        "spearman": spearman([r[0] for r in rows], [r[1] for r in rows]),
+        "neighbours": len(nb),
+        "pick_rank_in_neighbourhood": 1 + sum(meas[n] < pick[1] for n in nb),
+    }
+
+
+def gemm_markdown(summaries: list) -> str:
+    out = ["| M, N, K | candidates | planner pick (BM, BN, BK, WM, WN, pipe) | measured TFLOP/s "
+           "(modelled) | pick vs measured best | pick's measured rank | Spearman | pick's rank "
+           "among its block-size neighbours |", "|---|---|---|---|---|---|---|---|"]
+    for s in summaries:
+        out.append(f"| {s['shape']} | {s['candidates']} | {s['pick']} | {s['pick_tflops']:.0f} "
+                   f"({s['pick_modeled_tflops']:.0f}) | {s['pick_over_best']:+.1%} (best "
+                   f"{s['best']}) | {s['pick_measured_rank']} | {s['spearman']:.2f} | "
+                   f"{s['pick_rank_in_neighbourhood']} of {s['neighbours'] + 1} |")
+    return "\n".join(out)
+
+
+def main_gemm(a):
+    data = {}
+    if a.load:
+        with open(a.load) as f:
+            raw = json.load(f)
+        data = {tuple(map(int, s.split(","))): {tuple(map(int, k.split(","))): t
+                                               for k, t in m.items()} for s, m in raw.items()}
+    summaries = []
+    for shape in GEMM_SHAPES:
+        cands = pa.gemm_candidates(*shape)
+        if not a.load:
+            meas = {}
+            for c in cands:
+                meas[gemm_key(c)] = time_gemm(shape, gemm_key(c))
+                print(f"{shape} {gemm_key(c)} modelled {c['modeled_us']:.1f} us measured "
+                      f"{meas[gemm_key(c)]:.1f} us", flush=True)
+            data[shape] = meas
+        if shape in data:
+            summaries.append(gemm_summary(shape, cands, data[shape]))
+    if a.save:
+        with open(a.save, "w") as f:
+            json.dump({",".join(map(str, s)): {",".join(map(str, k)): t for k, t in m.items()}
+                       for s, m in data.items()}, f, indent=1)
+    text = gemm_markdown(summaries)
+    print(text)
+    if a.markdown:
+        with open(a.markdown, "w") as f:
+            f.write(text + "\n")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--save", help="write the measurements (JSON)")
     ap.add_argument("--load", help="reuse measurements (JSON) instead of timing")
     ap.add_argument("--fit", action="store_true", help="refit the calibrated description fields")
     ap.add_argument("--markdown", help="write the summary table here")
+    ap.add_argument("--gemm", action="store_true",
+                    help="the GEMM block-size ablation instead of the prefill one")
     a = ap.parse_args()
     import torch
     # torch's HIP runtime must initialise the device before this library's
     # first HIP call (the plan query below makes one)
     assert torch.cuda.is_available(), "the ablation needs a HIP device"
+    if a.gemm:
+        return main_gemm(a)
     data = {}
     if a.load:
         with open(a.load) as f:

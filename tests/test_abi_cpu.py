@@ -86,11 +86,31 @@ def test_decode_rejects_on_host(kw, code):
     assert pa.last_error() != ""
 
 
+def gemm(a=ALIGNED, b=ALIGNED, c=ALIGNED, M=16, N=16, K=16, flags=0):
+    return pa.lib.attn_gemm(a, b, c, M, N, K, flags)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(a=None), pa.ATTN_EINVAL),
+    (dict(c=ALIGNED + 4), pa.ATTN_EINVAL),
+    (dict(M=0), pa.ATTN_EINVAL),
+    (dict(N=-8), pa.ATTN_EINVAL),
+    (dict(flags=4), pa.ATTN_EINVAL),
+    (dict(K=12), pa.ATTN_EUNSUPPORTED),
+    (dict(N=20), pa.ATTN_EUNSUPPORTED),
+    (dict(M=1 << 20, K=1 << 10), pa.ATTN_EUNSUPPORTED),  # A is 2 GiB
+])
+def test_gemm_rejects_on_host(kw, code):
+    assert gemm(**kw) == code
+    assert pa.last_error() != ""
+
+
 @pytest.mark.skipif(HAS_GPU, reason="checks the no-device path")
 def test_valid_call_without_device_is_a_hip_error_not_a_fallback():
     assert fwd() == pa.ATTN_EHIP
     assert "device" in pa.last_error().lower() or "hip" in pa.last_error().lower()
     assert dec() == pa.ATTN_EHIP
+    assert gemm() == pa.ATTN_EHIP
 
 
 def test_stream_round_trip():

@@ -230,3 +230,58 @@ def test_key_split_model_charges_the_combine():
     for tile, times in by_tile.items():
         if 2 in times:
             assert times[2] > times[1] - 1e-9, tile
+
+
+# --------------------------------------------------------------------- GEMM
+GEMM_SHAPES = [(256, 256, 256), (1024, 1024, 1024), (4096, 4096, 4096), (16384, 256, 2048),
+               (256, 256, 16384), (8192, 8192, 8192), (300, 520, 1000)]
+
+
+@pytest.mark.parametrize("shape", GEMM_SHAPES)
+@pytest.mark.parametrize("b_nk", [False, True])
+def test_gemm_plan_is_the_argmin_of_its_candidates(shape, b_nk):
+    desc = spec()
+    M, N, K = shape
+    cands = pa.gemm_candidates(M, N, K, b_nk, desc=desc)
+    assert cands
+    best = min(c["modeled_us"] for c in cands)
+    p = pa.parse_plan(pa.gemm_plan(M, N, K, b_nk, desc=desc))
+    assert abs(p["modeled_us"] - best) <= 1e-3 * best
+    for c in cands:
+        assert c["lds_bytes"] <= desc.lds_bytes_per_cu
+        assert c["grid"] == -(-M // c["BLOCK_M"]) * -(-N // c["BLOCK_N"])
+        assert c["b_nk"] == int(b_nk)
+
+
+def test_gemm_double_buffer_trade_off():
+    # pipe 1 doubles the LDS footprint: never cheaper in LDS, never slower in
+    # the model when occupancy is unchanged (load latency hidden)
+    desc = spec()
+    cands = pa.gemm_candidates(8192, 8192, 8192, False, desc=desc)
+    by_tile = {}
+    for c in cands:
+        by_tile.setdefault((c["BLOCK_M"], c["BLOCK_N"], c["BLOCK_K"]), {})[c["PIPE"]] = c
+    for tile, pair in by_tile.items():
+        if 0 in pair and 1 in pair:
+            assert pair[1]["lds_bytes"] == 2 * pair[0]["lds_bytes"]
+            if pair[1]["wg_per_cu"] == pair[0]["wg_per_cu"]:
+                assert pair[1]["modeled_us"] <= pair[0]["modeled_us"] + 1e-9
+
+
+def test_gemm_big_tiles_for_big_shapes_small_tiles_for_small():
+    desc = spec()
+    big = pa.parse_plan(pa.gemm_plan(8192, 8192, 8192, desc=desc))
+    small = pa.parse_plan(pa.gemm_plan(256, 256, 256, desc=desc))
+    assert big["BLOCK_M"] * big["BLOCK_N"] > small["BLOCK_M"] * small["BLOCK_N"]
+    assert small["grid"] >= 4  # spread a small product over several CUs
+
+
+def test_gemm_model_bounds():
+    # never faster than the MFMA peak or the HBM traffic of A, B and C
+    desc = spec()
+    for M, N, K in GEMM_SHAPES:
+        for c in pa.gemm_candidates(M, N, K, False, desc=desc):
+            t = c["modeled_us"] * 1e-6
+            peak = desc.mfma_bf16_flops_per_clk_cu * desc.num_cus * desc.clock_ghz * 1e9
+            assert 2.0 * M * N * K / t <= peak * 1.0001
+            assert (2.0 * (M * K + K * N) + 4.0 * M * N) / t <= desc.hbm_bytes_per_s * 1.0001
