@@ -35,9 +35,14 @@
 // per cycle (two 16-lane groups 8 banks apart) cover all 64 banks.
 //
 // Tile loads.  Pipes 0, 1 and 3 load K/V tiles straight from global memory
-// into LDS (global_load_lds_dwordx4), with the K permutation and the padding
-// expressed in the per-lane source addresses; pipe 2 stages them through
-// registers.
+// into LDS (buffer_load_dwordx4 ... lds), with the K permutation and the
+// padding expressed in the per-lane source addresses; pipe 2 stages them
+// through registers.  With two slots (pipes 1 and 3) the LDS loads are
+// issued from inline assembly (lds_dma.h) and every workgroup barrier first
+// waits for the wave's own loads: issued through the compiler builtin, they
+// made the compiler hold reads of the current tile until the next tile's
+// loads had landed.  Pipe 0 has one slot, nothing to overlap, and keeps the
+// builtin.
 //
 // Pipelining (the HEG pipe knob, PIPE):
 //   0  one LDS slot per operand: load -> barrier -> compute -> barrier; any
@@ -66,6 +71,7 @@
 #include <type_traits>
 
 #include "common.h"
+#include "lds_dma.h"
 
 namespace attn {
 
@@ -158,6 +164,17 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     uint16_t* const kslot1 = lds + (NSLOT - 1) * L::K_TILE;
     uint16_t* const vslot0 = lds + NSLOT * L::K_TILE;
     uint16_t* const vslot1 = vslot0 + (NSLOT - 1) * L::V_TILE;
+
+    // Workgroup barrier.  Pipes 1 and 3 issue their LDS loads from inline
+    // assembly, which the compiler does not track: each wave first waits for
+    // its own loads, so the barrier publishes them.  Pipe 0 (one slot) and
+    // pipe 2 (stores from registers) keep the compiler's barrier.
+    auto tile_barrier = [&]() __attribute__((always_inline)) {
+        if constexpr (PIPE == 1 || PIPE == 3)
+            publish_barrier<0>();
+        else
+            __syncthreads();
+    };
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -285,12 +302,16 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     constexpr int KCH = BN * KST, VCH = BN * VST;                // positions per region
     constexpr int KI = (KCH + 63) / 64, VI = (VCH + 63) / 64;    // pieces per region
     constexpr int NJ = (KI + VI + NW - 1) / NW;  // pieces per wave (K pieces, then V)
-    constexpr int kRsrcFlags = 0x00020000;       // raw 32-bit buffer, gfx9 family
-    const int slab_bytes = Skv * D * 2;          // fits in 31 bits (checked by the host)
-    const __amdgpu_buffer_rsrc_t k_rsrc =
-        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(Kb), 0, slab_bytes, kRsrcFlags);
-    const __amdgpu_buffer_rsrc_t v_rsrc =
-        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(Vb), 0, slab_bytes, kRsrcFlags);
+    const uint32_t slab_bytes = (uint32_t)Skv * D * 2;  // fits in 31 bits (checked by the host)
+    const dma_rsrc_t k_rsrc = make_dma_rsrc(Kb, slab_bytes);
+    const dma_rsrc_t v_rsrc = make_dma_rsrc(Vb, slab_bytes);
+    constexpr int kRsrcFlags = 0x00020000;  // raw 32-bit buffer, gfx9 family
+    const __amdgpu_buffer_rsrc_t k_rsrc_b = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(Kb), 0, (int)slab_bytes, kRsrcFlags);
+    const __amdgpu_buffer_rsrc_t v_rsrc_b = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(Vb), 0, (int)slab_bytes, kRsrcFlags);
+    // LDS byte address of the slots: the array's, plus element offsets
+    const uint32_t lds_base = lds_address(lds);
     // Piece p (0 <= p < KI + VI) goes to wave p % NW: K pieces first, then V.
     // off[j]: byte offset inside a tile of this lane's source chunk for the
     // wave's j-th piece, -1 for none.
@@ -323,9 +344,15 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
             if (key0 + BN > Skv)  // ragged tile: rows past the end re-read the last key
                 o = ((min(key0 + o / (2 * D), Skv - 1) - key0) * D) * 2 + o % (2 * D);
             uint16_t* dst = is_k ? kdst + piece * 512 : vdst + (piece - KI) * 512;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                is_k ? k_rsrc : v_rsrc, (__attribute__((address_space(3))) void*)dst, 16, o,
-                key0 * D * 2, 0, 0);
+            if constexpr (PIPE == 0) {
+                // one slot: no read overlaps a load, the builtin's waits cost nothing
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    is_k ? k_rsrc_b : v_rsrc_b, (__attribute__((address_space(3))) void*)dst,
+                    16, o, key0 * D * 2, 0, 0);
+            } else {
+                lds_dma16(is_k ? k_rsrc : v_rsrc, lds_base + (uint32_t)(dst - lds) * 2, o,
+                          key0 * D * 2);
+            }
         }
     };
     auto dma_k = [&](int t, uint16_t* dst) __attribute__((always_inline)) {
@@ -569,7 +596,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     if (PIPE == 0) {
         two_loops(0, [&](int t, auto mask_tag) {
             dma(t, kslot0, t, vslot0);
-            __syncthreads();
+            tile_barrier();
             if (wave_active(t)) {
                 f32x16 s[KB];
                 bf16x8 pb[KB][2];
@@ -577,13 +604,13 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
                 probs(s, softmax_stats(s, t, mask_tag), pb);
                 pv(vslot0, pb);
             }
-            __syncthreads();
+            tile_barrier();
         });
     } else if (PIPE == 1) {
         // tile t+1 streams into the other slot while tile t is computed from
         // LDS; one barrier per tile
         dma(0, kslot0, 0, vslot0);
-        __syncthreads();
+        tile_barrier();
         two_loops(0, [&](int t, auto mask_tag) {
             const bool odd = t & 1;
             if (t + 1 < n_tiles) dma(t + 1, odd ? kslot0 : kslot1, t + 1, odd ? vslot0 : vslot1);
@@ -594,7 +621,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
                 probs(s, softmax_stats(s, t, mask_tag), pb);
                 pv(odd ? vslot1 : vslot0, pb);
             }
-            __syncthreads();
+            tile_barrier();
         });
     } else if (PIPE == 2) {
         // Ping-pong.  LDS holds K_t, K_{t+1} and V_{t-1}, V_t in two-slot
@@ -620,7 +647,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
             load_rows(Kb, 1, kr);
             store_k(kslot1, kr);
         }
-        __syncthreads();
+        tile_barrier();
         if (group_b && wave_active(0)) scores(kslot0, s);
         two_loops(0, [&](int t, auto mask_tag) {
             const bool odd = t & 1;
@@ -638,7 +665,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
             } else if (wave_active(t)) {
                 probs(s, softmax_stats(s, t, mask_tag), pb);
             }
-            __syncthreads();
+            tile_barrier();
             // phase 2
             if (!group_b) {
                 if (wave_active(t)) {
@@ -651,7 +678,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
             }
             if (t + 2 < n_tiles) store_k(k_t, kr);
             if (t + 1 < n_tiles) store_v(v_t1, vr);
-            __syncthreads();
+            tile_barrier();
         });
         if (pv_pending) pv(((n_tiles - 1) & 1) ? vslot1 : vslot0, pb);
     } else {
@@ -669,13 +696,13 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
         float mx_next = -INFINITY;  // row max of the next tile's scores
         dma(0, kslot0, 0, vslot0);
         if (n_tiles > 1) dma_k(1, kslot1);
-        __syncthreads();
+        tile_barrier();
         if (wave_active(0)) {
             scores(kslot0, sA);
             mx_next = first_masked <= 0 ? tile_max(sA, 0, std::true_type{})
                                         : tile_max(sA, 0, std::false_type{});
         }
-        __syncthreads();  // slot 0 takes K_2 at the end of iteration 0
+        tile_barrier();  // slot 0 takes K_2 at the end of iteration 0
 
         // Iteration t.  Its S(t+1) also runs on the last tile, against a stale
         // but finite K slot, and on a wave's first inactive tile; those scores
@@ -692,7 +719,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
                 mx_next = fused_tile(k_next, v_cur, s_cur, s_nxt, pb, t, m_ref, std::true_type{},
                                      mask_tag);
             }
-            __syncthreads();
+            tile_barrier();
         };
         // Two loops, one per masking mode of the next tile, each running two
         // tiles per trip (score sets A and B alternate).  The second loop
@@ -765,7 +792,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     // Pipes 0, 1 and 3 end every tile with a barrier, after which no wave
     // reads LDS, so the next q-tile may refill the slots at once; the
     // ping-pong schedule reads V once more after its last barrier.
-    if (PIPE == 2) __syncthreads();
+    if (PIPE == 2) tile_barrier();
     }  // pass
 }
 

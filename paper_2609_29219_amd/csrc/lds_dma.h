@@ -47,6 +47,14 @@ __device__ __forceinline__ uint32_t lds_address(const void* p) {
 #pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void lds_dma16(dma_rsrc_t rsrc, uint32_t lds_base, int voffset,
                                           int soffset) {
+    // the scalar operands are wave-uniform; readfirstlane puts them in SGPRs
+    // even where the compiler holds a uniform value in a VGPR
+    rsrc[0] = __builtin_amdgcn_readfirstlane(rsrc[0]);
+    rsrc[1] = __builtin_amdgcn_readfirstlane(rsrc[1]);
+    rsrc[2] = __builtin_amdgcn_readfirstlane(rsrc[2]);
+    rsrc[3] = __builtin_amdgcn_readfirstlane(rsrc[3]);
+    lds_base = __builtin_amdgcn_readfirstlane(lds_base);
+    soffset = __builtin_amdgcn_readfirstlane(soffset);
     asm volatile(
         "s_mov_b32 m0, %0\n\t"
         "s_nop 0\n\t"
