@@ -38,9 +38,13 @@ PROFILES = os.path.join(ROOT, "profiles")
 CSRC = os.path.join(ROOT, "paper_2609_29219_amd", "csrc")
 # sources that decide which kernel runs and what it does
 KERNEL_SOURCES = {
-    "prefill": ("fwd_kernel.h", "fwd_d128.hip", "fwd_d64.hip", "plan.cpp", "api.hip", "common.h"),
+    "prefill": ("fwd_kernel.h", "fwd_d128.hip", "fwd_d64.hip", "lds_dma.h", "plan.cpp", "api.hip",
+                "common.h"),
     "decode": ("decode.hip", "plan.cpp", "api.hip", "common.h"),
+    "gemm": ("gemm.hip", "lds_dma.h", "plan.cpp", "api.hip", "common.h"),
 }
+GEMM_WORKLOAD = "gemm_m8192_n8192_k8192"
+GEMM_SHAPE = (8192, 8192, 8192)
 
 
 def source_hash(kind: str) -> str:
@@ -156,6 +160,9 @@ def main():
 
     dev = "cuda:0"
     torch.cuda.set_device(0)
+    if a.config == GEMM_WORKLOAD:
+        print(json.dumps(gemm_leg(pa, dev, steps=a.steps, warmup=a.warmup)), flush=True)
+        return
     if a.config:
         w = BY_NAME[a.config]
         q, k, v, qd, kd, vd = _load_workload(w, dev)
@@ -248,11 +255,12 @@ def main():
     print(json.dumps(rec), flush=True)
 
 
-def gemm_leg(pa, dev, M=8192, N=8192, K=8192, steps=20, warmup=10) -> dict:
+def gemm_leg(pa, dev, steps=20, warmup=10) -> dict:
     """The GEMM workload (C = A B, bf16 in, fp32 out) timed on its own after
     the attention step, outside its timed region."""
     import torch
     from attn_inputs import random_bf16
+    M, N, K = GEMM_SHAPE
     a = random_bf16((M, K), 31).to(dev)
     b = random_bf16((K, N), 32).to(dev)
     c = torch.empty((M, N), dtype=torch.float32, device=dev)
@@ -267,11 +275,18 @@ def gemm_leg(pa, dev, M=8192, N=8192, K=8192, steps=20, warmup=10) -> dict:
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / steps
     tflops = 2.0 * M * N * K / (ms * 1e-3) / 1e12
-    return {"M": M, "N": N, "K": K, "value": tflops, "unit": "TFLOP/s", "ms_per_call": ms,
-            "plan": pa.gemm_plan(M, N, K),
+    return {"workload": GEMM_WORKLOAD, "M": M, "N": N, "K": K, "value": tflops,
+            "unit": "TFLOP/s", "ms_per_call": ms, "plan": pa.gemm_plan(M, N, K),
             "roofline": {"bound": "mfma", "achieved": tflops, "peak": PEAK_BF16_TFLOPS,
                          "unit": "TFLOP/s", "frac": tflops / PEAK_BF16_TFLOPS,
-                         "kernel": "gemm_kernel"}}
+                         "traffic": profiled_traffic("gemm", GEMM_WORKLOAD),
+                         "algorithmic_bytes": gemm_bytes(), "kernel": "gemm_kernel"}}
+
+
+def gemm_bytes() -> int:
+    """Algorithmic HBM bytes of the GEMM workload: A and B read once, C (fp32) written once."""
+    M, N, K = GEMM_SHAPE
+    return 2 * M * K + 2 * K * N + 4 * M * N
 
 
 if __name__ == "__main__":
