@@ -463,7 +463,7 @@ int attn_decode_ex(const void* q, const void* k, const void* v, float* o, float*
     }
     const float scale = (float)(1.0 / sqrt((double)d));
     const hipError_t e = launch_decode(plan, q, k, v, o, lse, static_cast<float*>(ws), B, Hq,
-                                       Hkv, Skv, scale, t_stream);
+                                       Hkv, Skv, scale, st->desc.num_xcds, t_stream);
     if (e != hipSuccess) return fail_hip(e, "decode launch");
     return ATTN_OK;
 }

@@ -37,6 +37,8 @@ struct DecodePlan {
     int threads = 0;   // threads per partial workgroup
     int unroll = 0;    // keys per lane group per loop step
     int heads_per_wg = 1;  // query heads of one key/value group served together
+    int mfma = 0;          // grouped-query kernel on the matrix cores (16 queries per workgroup)
+    int q_blocks = 1;      // query blocks of 16 per key/value head (matrix-core kernel)
     int wg_per_cu = 0;
     long long grid = 0;
     double modeled_us = 0.0;
@@ -76,6 +78,8 @@ constexpr int kFwdWaves[] = {4, 8};
 constexpr int kFwdPipe[] = {0, 1, 2, 3};  // 2 only with 8 waves, 3 only with BN <= 64
 constexpr int kDecodeThreads = 256;
 constexpr int kDecodeUnroll = 8;
+constexpr int kGqaWaves = 4;      // waves of a grouped-query (matrix-core) decode workgroup
+constexpr int kGqaMinGroup = 4;   // smallest group served by the matrix-core decode
 
 // LDS footprint of a prefill workgroup: K tile [BN][D+8] and V tile
 // [BN][D+32] in bf16, one slot each (pipe 0) or two (pipe 1, 2, 3).
@@ -173,7 +177,7 @@ hipError_t launch_split_combine(int d, const float* ws_m, const float* ws_l, con
                                 hipStream_t stream);
 hipError_t launch_decode(const DecodePlan& p, const void* q, const void* k, const void* v,
                          float* o, float* lse, float* workspace, int B, int Hq, int Hkv, int Skv,
-                         float scale, hipStream_t stream);
+                         float scale, int num_xcds, hipStream_t stream);
 hipError_t launch_gemm(const GemmPlan& p, const void* a, const void* b, void* c, int M, int N,
                        int K, int out_bf16, int num_xcds, hipStream_t stream);
 // Query heads of one key/value group that a decode workgroup serves together.

@@ -159,6 +159,223 @@ __global__ __launch_bounds__(NT) void decode_partial_kernel(
     }
 }
 
+// ---------------------------------------------------------------------------
+// Grouped-query decode on the matrix cores.  With G >= 4 query heads per
+// key/value head, each key is scored against G queries and each value row is
+// weighted G times: per key the work is a small dense product, which the
+// VALU kernel above cannot keep up with at HBM speed.  Here one workgroup
+// serves up to 16 query heads of one key/value head (queries padded to 16)
+// over one key split, as S^T = K Q^T and O^T += V^T P^T on
+// v_mfma_f32_16x16x32_bf16:
+//   * Q^T (B operand: 32 dims x 16 queries) stays in registers;
+//   * a wave takes 32 keys per step; K rows go from HBM straight into the A
+//     operand (16 keys x 32 dims, 16 bytes per lane).  The rows are
+//     permuted (block a holds keys 8g+0..3, block b keys 8g+4..7 in lane
+//     group g = lane/16), so the accumulators give lane (q, g) the scores of
+//     keys 8g..8g+7 of query q -- exactly the k-operand layout P^T needs;
+//   * V rows are staged in the wave's own LDS tile and read transposed with
+//     ds_read_b64_tr_b16 (A operand V^T: 16 dims x 32 keys);
+//   * per query an online softmax (max over the four lane groups by lane
+//     swaps), probabilities rounded to bf16 and the sum l over the rounded
+//     values (so the output is an exact convex combination of V rows);
+//   * the four waves merge through LDS and write the same unnormalised
+//     (m, l, o[d]) partials per (query head, split) as the kernel above.
+// Every memory operation is an ordinary load or LDS access the compiler
+// tracks; latency is hidden by occupancy (16 KiB in flight per wave).
+typedef __bf16 gq_bf16x8 __attribute__((ext_vector_type(8)));
+typedef float gq_f32x4 __attribute__((ext_vector_type(4)));
+typedef short gq_s16x4 __attribute__((ext_vector_type(4)));
+typedef short gq_s16x8 __attribute__((ext_vector_type(8)));
+
+// max / sum of x over the four 16-lane rows (lanes l, l^16, l^32, l^48)
+__device__ __forceinline__ float rows4_max(float x) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                    false);
+    x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                    false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float rows4_sum(float x) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                    false);
+    x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                    false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+template <int D>
+__global__ __launch_bounds__(kGqaWaves * 64) void gqa_decode_kernel(
+    const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
+    const uint16_t* __restrict__ V, float* __restrict__ ws_m, float* __restrict__ ws_l,
+    float* __restrict__ ws_o, int Hq, int Hkv, int Skv, int chunk, int n_splits, int q_blocks,
+    int n_wg, int num_xcds, float scale_log2) {
+    constexpr int KS = D / 32;        // MFMA k-steps over the head dimension
+    constexpr int DB = D / 16;        // 16-dim blocks of O^T
+    constexpr int VST = D + 32;       // bf16 per padded V row in LDS
+    constexpr int VCH = 32 * D / 8;   // 16-byte chunks of a 32-key V tile
+    constexpr int VI = VCH / 64;      // V chunks per lane
+    static_assert(VCH % 64 == 0, "whole V tile per wave");
+    __shared__ __attribute__((aligned(16))) uint16_t vtile[kGqaWaves][32 * VST];
+    __shared__ float sm[kGqaWaves][16], sl[kGqaWaves][16];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int l16 = lane & 15, g4 = lane >> 4;
+
+    // XCD-aware order: the query blocks of one key/value chunk are
+    // neighbours in the logical order and land on one XCD (shared K/V in L2)
+    const int wg = blockIdx.x;
+    const int per = n_wg / num_xcds, rem = n_wg % num_xcds;
+    const int xcd = wg % num_xcds, slot_id = wg / num_xcds;
+    const int logical =
+        (xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per) + slot_id;
+    const int qb = logical % q_blocks;
+    const int rest = logical / q_blocks;
+    const int split = rest % n_splits;
+    const long long kvh = rest / n_splits;  // flat b * Hkv + h
+    const int group = Hq / Hkv;
+    const long long b = kvh / Hkv;
+    const int q_first = (int)(kvh % Hkv) * group + qb * 16;  // first query head in batch b
+    const int nq = min(16, group - qb * 16);
+    const int j0 = split * chunk;
+    const int j1 = min(Skv, j0 + chunk);
+
+    // Q^T fragments: lane (q, g) holds dims 32s + 8g .. +7 of query q
+    gq_bf16x8 qf[KS];
+    {
+        const uint16_t* qp = Q + (b * Hq + q_first + min(l16, nq - 1)) * D + 8 * g4;
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+            u32x4 w = *reinterpret_cast<const u32x4*>(qp + 32 * s);
+            if (l16 >= nq) w = u32x4{0u, 0u, 0u, 0u};
+            qf[s] = __builtin_bit_cast(gq_bf16x8, w);
+        }
+    }
+    const uint16_t* Kb = K + kvh * (long long)Skv * D;
+    const uint16_t* Vb = V + kvh * (long long)Skv * D;
+    uint16_t* const vt = vtile[wave];
+    const int rk = 8 * (l16 >> 2) + (l16 & 3);  // this lane's K row inside block a
+
+    float m = -INFINITY, l = 0.f;
+    gq_f32x4 oacc[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) oacc[db] = gq_f32x4{0.f, 0.f, 0.f, 0.f};
+
+    for (int kb = j0 + 32 * wave; kb < j1; kb += 32 * kGqaWaves) {
+        // keys past the split end re-read the last key (masked to weight 0)
+        u32x4 kr[2][KS], vr[VI];
+#pragma unroll
+        for (int blk = 0; blk < 2; ++blk) {
+            const int key = min(kb + rk + 4 * blk, j1 - 1);
+#pragma unroll
+            for (int s = 0; s < KS; ++s)
+                kr[blk][s] = __builtin_nontemporal_load(
+                    reinterpret_cast<const u32x4*>(Kb + (long long)key * D + 32 * s + 8 * g4));
+        }
+#pragma unroll
+        for (int i = 0; i < VI; ++i) {
+            const int c = lane + 64 * i, row = c / (D / 8), cc = c % (D / 8);
+            const int key = min(kb + row, j1 - 1);
+            vr[i] = __builtin_nontemporal_load(
+                reinterpret_cast<const u32x4*>(Vb + (long long)key * D + cc * 8));
+        }
+        // this wave's V tile (its earlier reads of the tile precede these
+        // writes in the wave's LDS order)
+#pragma unroll
+        for (int i = 0; i < VI; ++i) {
+            const int c = lane + 64 * i, row = c / (D / 8), cc = c % (D / 8);
+            *reinterpret_cast<u32x4*>(vt + row * VST + cc * 8) = vr[i];
+        }
+        // scores: lane (q, g) gets keys kb + 8g + e, e = 0..7
+        gq_f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+            sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(gq_bf16x8, kr[0][s]),
+                                                        qf[s], sa, 0, 0, 0);
+            sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(gq_bf16x8, kr[1][s]),
+                                                        qf[s], sb, 0, 0, 0);
+        }
+        float sc[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            sc[i] = sa[i];
+            sc[4 + i] = sb[i];
+        }
+        const int room = j1 - 1 - (kb + 8 * g4);  // keys e <= room exist
+        float mx = -INFINITY;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            if (e > room) sc[e] = -INFINITY;
+            mx = fmaxf(mx, sc[e]);
+        }
+        mx = rows4_max(mx);  // key kb always exists: finite
+        const float m_new = fmaxf(m, mx * scale_log2);
+        const float alpha = __builtin_amdgcn_exp2f(m - m_new);
+        l *= alpha;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) oacc[db] *= alpha;
+        m = m_new;
+        gq_bf16x8 pf;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            pf[e] = (__bf16)__builtin_amdgcn_exp2f(fmaf(sc[e], scale_log2, -m));
+            l += (float)pf[e];
+        }
+        // O^T += V^T P^T: lane (i, g) of a 16-lane group reads row 8g + i/4
+        // (and + 4) at column 16 db + 4 (i % 4), and receives column
+        // 16 db + i of keys 8g .. 8g+3 (and 8g+4 .. 8g+7)
+        const uint16_t* vp = vt + (8 * g4 + (l16 >> 2)) * VST + 4 * (l16 & 3);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+            const gq_s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) gq_s16x4*)(vp + 16 * db));
+            const gq_s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) gq_s16x4*)(vp + 4 * VST + 16 * db));
+            const gq_s16x8 w = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+            oacc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(gq_bf16x8, w),
+                                                              pf, oacc[db], 0, 0, 0);
+        }
+    }
+    l = rows4_sum(l);  // the four lane groups summed different keys
+
+    // merge the waves: O^T of wave w into LDS (over its V tile), then one
+    // thread per (query, dim)
+    __syncthreads();
+    float* so = reinterpret_cast<float*>(&vtile[0][0]);  // [wave][D][16]
+    static_assert(kGqaWaves * D * 16 * 4 <= (int)sizeof(vtile), "merge buffer fits");
+    if (g4 == 0) {
+        sm[wave][l16] = m;
+        sl[wave][l16] = l;
+    }
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) so[(wave * D + 16 * db + 4 * g4 + i) * 16 + l16] = oacc[db][i];
+    __syncthreads();
+    for (int idx = tid; idx < nq * D; idx += kGqaWaves * 64) {
+        const int q = idx / D, c = idx % D;
+        float M = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < kGqaWaves; ++w) M = fmaxf(M, sm[w][q]);
+        float L = 0.f, acc = 0.f;
+#pragma unroll
+        for (int w = 0; w < kGqaWaves; ++w) {
+            const float wt = __builtin_amdgcn_exp2f(sm[w][q] - M);  // waves without keys: 0
+            L = fmaf(wt, sl[w][q], L);
+            acc = fmaf(wt, so[(w * D + c) * 16 + q], acc);
+        }
+        const long long out = (b * Hq + q_first + q) * n_splits + split;
+        ws_o[out * D + c] = acc;
+        if (c == 0) {
+            ws_m[out] = M;
+            ws_l[out] = L;
+        }
+    }
+}
+
 // Global softmax over the split partials and the final output:
 //   M = max_s m_s, w_s = 2^(m_s - M), o = sum_s w_s o_s / sum_s w_s l_s,
 // and optionally the log-sum-exp of the row's scores (natural log),
@@ -226,13 +443,24 @@ static hipError_t launch_partial(const DecodePlan& p, const void* q, const void*
 template <int D>
 static hipError_t launch_decode_d(const DecodePlan& p, const void* q, const void* k,
                                   const void* v, float* o, float* lse, float* ws, int B, int Hq,
-                                  int Hkv, int Skv, float scale_log2, hipStream_t st) {
+                                  int Hkv, int Skv, float scale_log2, int num_xcds,
+                                  hipStream_t st) {
     const long long BHq = (long long)B * Hq;
     const int group = Hq / Hkv;
     float* ws_m = ws;
     float* ws_l = ws + BHq * p.n_splits;
     float* ws_o = ws + 2 * BHq * p.n_splits;
     hipError_t e = hipErrorInvalidValue;
+    if (p.mfma) {
+        if (p.grid > 0x7fffffffLL || p.q_blocks != (group + 15) / 16) return hipErrorInvalidValue;
+        hipLaunchKernelGGL((gqa_decode_kernel<D>), dim3((unsigned)p.grid), dim3(kGqaWaves * 64), 0,
+                           st, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                           static_cast<const uint16_t*>(v), ws_m, ws_l, ws_o, Hq, Hkv, Skv,
+                           p.chunk, p.n_splits, p.q_blocks, (int)p.grid, num_xcds, scale_log2);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        return launch_split_combine(D, ws_m, ws_l, ws_o, o, 0, lse, BHq, p.n_splits, st);
+    }
     switch (decode_heads_per_wg(group)) {
         case 8: e = launch_partial<D, 8>(p, q, k, v, ws_m, ws_l, ws_o, BHq, Skv, group, scale_log2, st); break;
         case 4: e = launch_partial<D, 4>(p, q, k, v, ws_m, ws_l, ws_o, BHq, Skv, group, scale_log2, st); break;
@@ -245,12 +473,14 @@ static hipError_t launch_decode_d(const DecodePlan& p, const void* q, const void
 
 hipError_t launch_decode(const DecodePlan& p, const void* q, const void* k, const void* v,
                          float* o, float* lse, float* workspace, int B, int Hq, int Hkv, int Skv,
-                         float scale, hipStream_t stream) {
+                         float scale, int num_xcds, hipStream_t stream) {
     const float scale_log2 = (float)((double)scale * 1.4426950408889634);
     if (p.d == 64)
-        return launch_decode_d<64>(p, q, k, v, o, lse, workspace, B, Hq, Hkv, Skv, scale_log2, stream);
+        return launch_decode_d<64>(p, q, k, v, o, lse, workspace, B, Hq, Hkv, Skv, scale_log2,
+                                   num_xcds, stream);
     if (p.d == 128)
-        return launch_decode_d<128>(p, q, k, v, o, lse, workspace, B, Hq, Hkv, Skv, scale_log2, stream);
+        return launch_decode_d<128>(p, q, k, v, o, lse, workspace, B, Hq, Hkv, Skv, scale_log2,
+                                    num_xcds, stream);
     return hipErrorInvalidValue;
 }
 

@@ -466,15 +466,28 @@ bool plan_decode(const attn_device_desc& desc, int B, int Hq, int Hkv, int Skv, 
                  DecodePlan* out) {
     if (Hkv <= 0 || Hq % Hkv != 0) return false;
     // query heads sharing a key/value head run in one workgroup, which reads
-    // each K/V chunk once for all of them
-    const int gq = decode_heads_per_wg(Hq / Hkv);
-    const int nt = kDecodeThreads, unroll = gq >= 4 ? 4 : kDecodeUnroll;
-    const int groups = nt / (d / 8);       // keys per workgroup step
-    const int step_keys = groups * unroll;  // keys per loop iteration
-    const long long BH = (long long)B * Hq / gq;  // key/value streams
+    // each K/V chunk once for all of them.  From kGqaMinGroup heads on, the
+    // per-key work is a small dense product and runs on the matrix cores
+    // (16 queries per workgroup, 32 keys per wave step, K and V of a step in
+    // flight per wave); below, the VALU kernel (GQ heads per workgroup).
+    const int group = Hq / Hkv;
+    const bool mfma = group >= kGqaMinGroup;
+    const int q_blocks = mfma ? (group + 15) / 16 : 1;
+    const int gq = mfma ? std::min(group, 16) : decode_heads_per_wg(group);
+    const int nt = mfma ? kGqaWaves * 64 : kDecodeThreads;
+    const int unroll = mfma ? 1 : (gq >= 4 ? 4 : kDecodeUnroll);
+    const int step_keys = mfma ? 32 * kGqaWaves : nt / (d / 8) * unroll;  // keys per loop trip
+    // workgroups per split: key/value streams (times query blocks)
+    const long long BH = mfma ? (long long)B * Hkv * q_blocks : (long long)B * Hq / gq;
     const long long BHq = (long long)B * Hq;
     const double cu_share = desc.hbm_bytes_per_s / desc.num_cus;  // bytes/s per CU
-    const int max_wg_cu = std::max(1, desc.max_waves_per_simd * desc.simds_per_cu / (nt / 64));
+    int max_wg_cu = std::max(1, desc.max_waves_per_simd * desc.simds_per_cu / (nt / 64));
+    if (mfma)  // LDS: one padded 32-key V tile per wave
+        max_wg_cu = std::min(max_wg_cu, desc.lds_bytes_per_cu / (kGqaWaves * 32 * (d + 32) * 2 +
+                                                                  2 * kGqaWaves * 16 * 4));
+    // bytes a workgroup keeps in flight: VALU kernel 2*unroll 16-byte loads
+    // per lane; matrix-core kernel one step's K and V per wave
+    const double wg_inflight = mfma ? (double)kGqaWaves * 32 * d * 4 : nt * 2.0 * unroll * 16.0;
 
     auto model = [&](int n, DecodePlan* p) -> bool {
         const int chunk = (Skv + n - 1) / n;
@@ -484,8 +497,7 @@ bool plan_decode(const attn_device_desc& desc, int B, int Hq, int Hkv, int Skv, 
         const double wg_bytes = (double)chunk * d * 4.0;
         const double per_cu = ceil((double)grid / desc.num_cus);  // workgroups per CU
         const double resident = std::min<double>(per_cu, max_wg_cu);
-        // bytes in flight per CU: every lane keeps 2*unroll 16-byte loads open
-        const double inflight = resident * nt * 2.0 * unroll * 16.0;
+        const double inflight = resident * wg_inflight;  // bytes in flight per CU
         const double cu_bw = std::min(cu_share, inflight / (desc.hbm_latency_us * 1e-6));
         // for(steps, pipe(load, local softmax)): load-bound, loads overlap compute
         const double steps = ceil((double)chunk / step_keys);
@@ -500,6 +512,8 @@ bool plan_decode(const attn_device_desc& desc, int B, int Hq, int Hkv, int Skv, 
         p->threads = nt;
         p->unroll = unroll;
         p->heads_per_wg = gq;
+        p->mfma = mfma ? 1 : 0;
+        p->q_blocks = q_blocks;
         p->wg_per_cu = (int)resident;
         p->grid = grid;
         p->modeled_us = desc.launch_us + stream_us + merge_us + combine_us;
@@ -554,10 +568,9 @@ int format_fwd_plan(const FwdPlan& p, char* buf, int buflen) {
 int format_decode_plan(const DecodePlan& p, char* buf, int buflen) {
     return snprintf(buf, buf ? (size_t)buflen : 0,
                     "kind=decode d=%d N_SPLITS=%d CHUNK=%d THREADS=%d UNROLL=%d HEADS_PER_WG=%d "
-                    "grid=%lld wg_per_cu=%d modeled_us=%.3f bound=%s",
-                    p.d, p.n_splits, p.chunk, p.threads, p.unroll, p.heads_per_wg, p.grid,
-                    p.wg_per_cu,
-                    p.modeled_us, p.bound);
+                    "MFMA=%d Q_BLOCKS=%d grid=%lld wg_per_cu=%d modeled_us=%.3f bound=%s",
+                    p.d, p.n_splits, p.chunk, p.threads, p.unroll, p.heads_per_wg, p.mfma,
+                    p.q_blocks, p.grid, p.wg_per_cu, p.modeled_us, p.bound);
 }
 
 }  // namespace attn

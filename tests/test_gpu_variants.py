@@ -117,13 +117,18 @@ def test_fwd_ex_rejects_before_launch(pa):
     assert e.value.code == pa.ATTN_EINVAL
 
 
-DECODE_GQA = [  # B, Hq, Hkv, Skv, d, n_splits
+DECODE_GQA = [  # B, Hq, Hkv, Skv, d, n_splits  (group >= 4: the matrix-core kernel)
     (2, 8, 2, 1000, 128, 0),
     (1, 32, 4, 4096, 128, 0),
     (3, 6, 2, 777, 64, 5),
     (1, 16, 1, 2049, 128, 0),
     (2, 12, 4, 300, 128, 3),
     (1, 32, 2, 8192, 64, 0),
+    (2, 32, 1, 1500, 128, 0),   # MQA: two query blocks of 16
+    (1, 48, 2, 700, 128, 4),    # group 24: a full and a partial query block
+    (3, 8, 2, 33, 128, 0),      # fewer keys than one 32-key step per wave
+    (2, 20, 4, 1, 64, 0),       # a single key
+    (1, 64, 8, 65536, 128, 0),  # long context, group 8
 ]
 
 
@@ -139,8 +144,53 @@ def test_decode_gqa_lse(pa, shape):
     ref, ref_lse = oracle.attn_gqa(q.reshape(B, Hq, 1, d).contiguous(), k, v, B, Hq, Hkv, 1, Skv,
                                    d, sc, False)
     compare(o, ref.reshape(B, Hq, d), f"decode gqa {shape}")
-    # decode sums unrounded fp32 probabilities: the lse is fp32-accurate
-    compare(lse, ref_lse.reshape(B, Hq), f"decode gqa lse {shape}", max_abs=1e-4, mean_abs=2e-5)
+    if Hq // Hkv < 4:
+        # the VALU kernel sums unrounded fp32 probabilities: fp32-accurate lse
+        compare(lse, ref_lse.reshape(B, Hq), f"decode gqa lse {shape}", max_abs=1e-4,
+                mean_abs=2e-5)
+    else:
+        # the matrix-core kernel sums the bf16-rounded probabilities (as prefill)
+        compare(lse, ref_lse.reshape(B, Hq), f"decode gqa lse {shape}", max_abs=LSE_MAX_ABS,
+                mean_abs=LSE_MEAN_ABS)
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_decode_gqa_closed_forms(pa, d):
+    # matrix-core decode: identical V rows give that row exactly (the weights
+    # are an exact convex combination); Q = 0 gives the column mean of V and
+    # lse = log(Skv)
+    B, Hq, Hkv, Skv = 2, 16, 2, 777
+    q = random_bf16((B, Hq, d), 1600)
+    k = random_bf16((B, Hkv, Skv, d), 1601)
+    row = random_bf16((B, Hkv, 1, d), 1602)
+    v_same = row.expand(B, Hkv, Skv, d).contiguous()
+    announce(f"attn_decode_ex gqa closed forms d={d}")
+    o = pa.attn_decode(q.to(DEV), k.to(DEV), v_same.to(DEV))
+    v = random_bf16((B, Hkv, Skv, d), 1603)
+    o0, lse0 = pa.attn_decode(torch.zeros_like(q).to(DEV), k.to(DEV), v.to(DEV), return_lse=True)
+    torch.cuda.synchronize()
+    want = row.float().repeat_interleave(Hq // Hkv, dim=1).reshape(B, Hq, d)
+    np.testing.assert_allclose(o.cpu().double().numpy(), want.double().numpy(), atol=2e-6,
+                               rtol=1e-6)
+    mean = v.double().mean(dim=2).repeat_interleave(Hq // Hkv, dim=1)
+    compare(o0, mean.numpy(), "Q = 0 gives the mean of V", max_abs=2e-3, mean_abs=2e-4)
+    np.testing.assert_allclose(lse0.cpu().double().numpy(), math.log(Skv), atol=2e-6, rtol=0)
+
+
+def test_decode_gqa_split_invariance(pa):
+    B, Hq, Hkv, Skv, d = 1, 16, 2, 5000, 128
+    q = random_bf16((B, Hq, d), 1700).to(DEV)
+    k = random_bf16((B, Hkv, Skv, d), 1701).to(DEV)
+    v = random_bf16((B, Hkv, Skv, d), 1702).to(DEV)
+    announce("attn_decode_ex gqa split counts")
+    outs = {n: pa.attn_decode(q, k, v, n_splits=n) for n in (1, 3, 16, 40)}
+    torch.cuda.synchronize()
+    ref, _ = oracle.attn_gqa(q.cpu().reshape(B, Hq, 1, d).contiguous(), k.cpu(), v.cpu(), B, Hq,
+                             Hkv, 1, Skv, d, float(np.float32(1.0 / math.sqrt(d))), False)
+    for n, o in outs.items():
+        compare(o, ref.reshape(B, Hq, d), f"splits {n} vs oracle")
+        # the splits change only which reference max each probability is rounded against
+        compare(o, outs[1].cpu().double().numpy(), f"splits {n} vs 1", max_abs=2e-3, mean_abs=2e-4)
 
 
 def test_decode_caller_workspace(pa):
