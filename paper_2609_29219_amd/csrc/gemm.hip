@@ -46,6 +46,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "common.h"
 #include "lds_dma.h"
 
@@ -139,34 +141,40 @@ void gemm_kernel(const GemmArgs args) {
     // Piece p (0 <= p < NP) goes to wave p % NW: A pieces first, then B.
     // off[j]: byte offset of this lane's source chunk for the wave's j-th
     // piece, relative to the k-tile's first element (the tile-dependent part
-    // is the scalar offset); kof[j]: the chunk's k offset inside the tile
-    // (for the ragged end of K).
-    int off[NJ], kof[NJ];
+    // is the scalar offset).  kof(j): the chunk's k offset inside the tile,
+    // recomputed on the ragged last k-tile only.
+    int off[NJ];
+    auto pos_of = [&](int j) __attribute__((always_inline)) {
+        const int piece = wave + j * NW;
+        return (piece < L::A_PIECES ? piece : piece - L::A_PIECES) * 64 + lane;
+    };
+    auto kof = [&](int j) __attribute__((always_inline)) -> int {
+        const int pos = pos_of(j);
+        if (wave + j * NW < L::A_PIECES) return min(pos % L::A_CPR, L::A_REAL - 1) * 8;
+        if (B_NK) return min(pos % L::B_CPR, L::B_REAL - 1) * 8;
+        return pos / L::B_CPR;
+    };
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
         const int piece = wave + j * NW;
         const bool is_a = piece < L::A_PIECES;
-        const int pos = (is_a ? piece : piece - L::A_PIECES) * 64 + lane;
-        int o = 0, kk = 0;
+        const int pos = pos_of(j);
+        int o = 0;
         if (is_a) {
             const int r = pos / L::A_CPR, c = min(pos % L::A_CPR, L::A_REAL - 1);
             const int row = min(m0 + r, M - 1) - m0;
             o = (row * K + c * 8) * 2;
-            kk = c * 8;
         } else if (B_NK) {
             const int r = pos / L::B_CPR, c = min(pos % L::B_CPR, L::B_REAL - 1);
             const int row = min(n0 + r, N - 1) - n0;
             o = (row * K + c * 8) * 2;
-            kk = c * 8;
         } else {
             // columns past N (outputs never stored) re-read the last chunk of the row
             const int c = min(min(pos % L::B_CPR, L::B_REAL - 1), (N - n0) / 8 - 1);
             const int r = pos / L::B_CPR;
             o = (r * N + c * 8) * 2;
-            kk = r;
         }
         off[j] = o;
-        kof[j] = kk;
     }
     // Issue this wave's pieces of k-tile t into LDS slot s (NJ_MIN or NJ
     // loads; the branches are wave-uniform).
@@ -182,7 +190,7 @@ void gemm_kernel(const GemmArgs args) {
             const int piece = wave + j * NW;
             if (piece >= NP) continue;
             const bool is_a = piece < L::A_PIECES;
-            const int o = (ragged && kof[j] >= K - k0) ? oob : off[j];
+            const int o = (ragged && kof(j) >= K - k0) ? oob : off[j];
             if (is_a)
                 lds_dma16(a_rsrc, a_dst + piece * 1024, o, a_base);
             else
@@ -280,33 +288,45 @@ void gemm_kernel(const GemmArgs args) {
         }
     }
 
-    // ---- epilogue: lane (m, h) writes 4 consecutive columns per register group
+    // ---- epilogue: lane (m, h) writes 4 consecutive columns per register group;
+    // one accumulator block at a time (the output type is decided outside the
+    // loops), so a wave holding 256 accumulators never needs them all in VGPRs
     const int m = m0 + wm0 + l32;  // + 32 * mb
+    auto store_all = [&](auto bf16_tag) __attribute__((always_inline)) {
+        constexpr bool BF16 = decltype(bf16_tag)::value;
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-        const int row = m + mb * 32;
-        if (row >= M) continue;
+        for (int mb = 0; mb < MB; ++mb) {
+            const int row = m + mb * 32;
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
+            for (int nb = 0; nb < NB; ++nb) {
+                if (row < M) {
 #pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const int col = n0 + wn0 + nb * 32 + 8 * g + 4 * hh;
-                if (col >= N) continue;
-                const g_f32x16& c = acc[nb][mb];
-                if (args.out_bf16) {
-                    const g_bf16x2 lo = {(__bf16)c[4 * g], (__bf16)c[4 * g + 1]};
-                    const g_bf16x2 hi = {(__bf16)c[4 * g + 2], (__bf16)c[4 * g + 3]};
-                    const uint2 w = {__builtin_bit_cast(uint32_t, lo),
-                                     __builtin_bit_cast(uint32_t, hi)};
-                    *reinterpret_cast<uint2*>(static_cast<uint16_t*>(args.c) +
-                                              (long long)row * N + col) = w;
-                } else {
-                    const float4 v = {c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]};
-                    *reinterpret_cast<float4*>(static_cast<float*>(args.c) + (long long)row * N +
-                                               col) = v;
+                    for (int g = 0; g < 4; ++g) {
+                        const int col = n0 + wn0 + nb * 32 + 8 * g + 4 * hh;
+                        if (col >= N) continue;
+                        const g_f32x16& c = acc[nb][mb];
+                        if constexpr (BF16) {
+                            const g_bf16x2 lo = {(__bf16)c[4 * g], (__bf16)c[4 * g + 1]};
+                            const g_bf16x2 hi = {(__bf16)c[4 * g + 2], (__bf16)c[4 * g + 3]};
+                            const uint2 w = {__builtin_bit_cast(uint32_t, lo),
+                                             __builtin_bit_cast(uint32_t, hi)};
+                            *reinterpret_cast<uint2*>(static_cast<uint16_t*>(args.c) +
+                                                      (long long)row * N + col) = w;
+                        } else {
+                            const float4 v = {c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]};
+                            *reinterpret_cast<float4*>(static_cast<float*>(args.c) +
+                                                       (long long)row * N + col) = v;
+                        }
+                    }
                 }
+                __builtin_amdgcn_sched_barrier(0);
             }
-    }
+        }
+    };
+    if (args.out_bf16)
+        store_all(std::true_type{});
+    else
+        store_all(std::false_type{});
 }
 
 template <int BM, int BN, int BK, bool B_NK, int PIPE>
