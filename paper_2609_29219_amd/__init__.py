@@ -287,15 +287,17 @@ def get_plan(kind: int, B: int, H: int, Sq: int, Skv: int, d: int, causal: bool 
 
 
 def fwd_candidates(B: int, H: int, Sq: int, Skv: int, d: int, causal: bool = False,
-                   desc: DeviceDesc | None = None, device_footprint: bool = False) -> list[dict]:
+                   desc: DeviceDesc | None = None, device_footprint: bool = False,
+                   analytic_only: bool = False) -> list[dict]:
     """Every feasible prefill candidate with its modelled time (not ABI; for
     the block-size ablation).  desc None: this device's description and the
     compiled kernels' real register/occupancy footprint; with a desc, the
-    footprint is estimated unless device_footprint is set."""
+    footprint is estimated unless device_footprint is set.  analytic_only:
+    without the measured per-variant tile costs."""
     buf = ctypes.create_string_buffer(1 << 18)
     ptr = ctypes.byref(desc) if desc is not None else None
-    rc = lib.attn__fwd_candidates(ptr, B, H, Sq, Skv, d, int(bool(causal)),
-                                  int(bool(device_footprint)), buf, 1 << 18)
+    flags = int(bool(device_footprint)) | (2 if analytic_only else 0)
+    rc = lib.attn__fwd_candidates(ptr, B, H, Sq, Skv, d, int(bool(causal)), flags, buf, 1 << 18)
     if rc < 0:
         raise AttnError(rc, last_error())
     return [parse_plan(l) for l in buf.value.decode().splitlines() if l.strip()]

@@ -314,7 +314,13 @@ int attn__fwd_candidates(const attn_device_desc* desc, int B, int H, int Sq, int
     attn_device_desc local;
     FwdResFn res = nullptr;
     const bool have = attn_query_device(&local) == ATTN_OK && strcmp(local.arch, "gfx950") == 0;
-    if (have && (device_footprint || !desc)) res = fwd_resources;
+    // bit 0: the compiled kernels' real footprint; bit 1: the analytic model
+    // without the measured per-variant tile costs
+    if (have && ((device_footprint & 1) || !desc)) res = fwd_resources;
+    struct Scales {
+        explicit Scales(bool on) { use_fwd_primitive_costs(on); }
+        ~Scales() { use_fwd_primitive_costs(true); }
+    } scales(!(device_footprint & 2));
     if (!desc) desc = &local;
     if (buflen < 0 || (buflen > 0 && !buf)) return fail(ATTN_EINVAL, "bad output buffer");
     if (B <= 0 || H <= 0 || Sq <= 0 || Skv <= 0) return fail(ATTN_EINVAL, "bad dimensions");

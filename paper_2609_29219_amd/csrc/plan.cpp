@@ -28,6 +28,7 @@
 #include <algorithm>
 
 #include "common.h"
+#include "fwd_primitives.inc"
 
 namespace attn {
 
@@ -118,6 +119,20 @@ int fwd_vgprs(int d, int bn, int waves, int pipe) {
 // times, the partials (d + 2 floats per row and split) written and read back,
 // and a second launch (the split combine, the same global-softmax step as
 // decode's).
+// Per-variant tile-cost factors (the compiled tile kernels characterised
+// once on gfx950, fwd_primitives.inc); a thread may switch them off to see
+// the analytic model alone (the calibration script does).
+static thread_local bool t_prim_scales = true;
+void use_fwd_primitive_costs(bool on) { t_prim_scales = on; }
+static double fwd_prim_scale(int d, int bn, int waves, int pipe, int causal) {
+    const int di = d == 128 ? 1 : 0;
+    const int bi = bn == 32 ? 0 : bn == 64 ? 1 : 2;
+    const int wi = waves == 8 ? 1 : 0;
+    if (!t_prim_scales || (d != 64 && d != 128) || pipe < 0 || pipe > 3) return 1.0;
+    const double f = kFwdPrimScale[di][bi][wi][pipe][causal ? 1 : 0];
+    return f > 0.0 ? f : 1.0;
+}
+
 bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d,
                     int causal, int bn, int waves, int pipe, FwdPlan* out, FwdResFn res,
                     int kv_splits) {
@@ -179,7 +194,9 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
     const double body = std::max(compute, lds);
     const double latency = desc.tile_latency_cycles;
     // pipe node (load, body, -): knob b_lm open for pipe >= 1
-    const double tile = heg_pipe(latency / wg, body, 0.0, pipe >= 1 ? 1 : 0, 0);
+    // the compiled kernel's measured cost relative to this analytic body
+    const double tile = heg_pipe(latency / wg, body, 0.0, pipe >= 1 ? 1 : 0, 0) *
+                        fwd_prim_scale(d, bn, waves, pipe, causal);
     const double load_q = latency;
 
     // ---- grid: regular (non-causal) or regularised (causal) --------------
