@@ -248,13 +248,15 @@ def gemm_plan(M: int, N: int, K: int, b_nk: bool = False, desc: DeviceDesc | Non
 
 
 def gemm_candidates(M: int, N: int, K: int, b_nk: bool = False, desc: DeviceDesc | None = None,
-                    device_footprint: bool = False) -> list[dict]:
+                    device_footprint: bool = False, analytic_only: bool = False) -> list[dict]:
     """Every feasible GEMM candidate with its modelled time (not ABI; for the
-    block-size ablation)."""
+    block-size ablation).  analytic_only: without the measured per-variant
+    costs."""
     buf = ctypes.create_string_buffer(1 << 16)
     ptr = ctypes.byref(desc) if desc is not None else None
-    rc = lib.attn__gemm_candidates(ptr, M, N, K, ATTN_GEMM_B_NK if b_nk else 0,
-                                   int(bool(device_footprint)), buf, 1 << 16)
+    flags = int(bool(device_footprint)) | (2 if analytic_only else 0)
+    rc = lib.attn__gemm_candidates(ptr, M, N, K, ATTN_GEMM_B_NK if b_nk else 0, flags, buf,
+                                   1 << 16)
     if rc < 0:
         raise AttnError(rc, last_error())
     return [parse_plan(l) for l in buf.value.decode().splitlines() if l.strip()]

@@ -1,6 +1,6 @@
 """Characterise the compiled prefill tile kernels once on a gfx950 device.
 
-    python paper_2609_29219_amd/calibrate_primitives.py [--write [--out FILE]]
+    python paper_2609_29219_amd/calibrate_primitives.py [--gemm] [--write [--out FILE]]
 
 For each head dimension and masking mode, every valid tile variant (block
 width, waves, pipeline knob) is timed on one calibration shape -- B1 H32
@@ -10,11 +10,15 @@ is the variant's per-tile cost factor: the planner multiplies the modelled
 tile cost by it.  This is the paper's primitive characterisation (its
 latency model takes the cost of each primitive from isolated measurements,
 collected once per architecture), applied to the compiled tile kernels; no
-shape is tuned.  --write regenerates csrc/fwd_primitives.inc.
+shape is tuned.  --write regenerates csrc/fwd_primitives.inc.  --gemm does the
+same for the GEMM tile kernels (each B layout and pipe setting, alone on a CU
+-- one tile per CU, K = 8192 -- and sharing CUs at M = N = K = 4096) into
+csrc/gemm_primitives.inc.
 """
 from __future__ import annotations
 
 import argparse
+import ctypes
 import os
 import sys
 
@@ -49,13 +53,96 @@ def time_variant(q, k, v, o, causal, bn, nw, pipe, iters=10, reps=3) -> float:
         os.environ.pop("ATTN_FORCE_PLAN", None)
 
 
+GEMM_SHAPE = (4096, 4096, 4096)
+GEMM_INC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc", "gemm_primitives.inc")
+# the planner's kGemmTiles order: (BM, BN, BK, WM, WN)
+GEMM_TILES = [(64, 64, 64, 2, 2), (128, 128, 32, 2, 2), (128, 128, 64, 2, 2),
+              (256, 128, 32, 2, 2), (256, 128, 64, 2, 2), (128, 256, 32, 2, 2),
+              (128, 256, 64, 2, 2), (256, 256, 32, 2, 4), (256, 256, 64, 2, 4)]
+
+
+def time_gemm_tile(a, b, c, b_nk, tile, pipe) -> float:
+    import torch
+    os.environ["ATTN_FORCE_GEMM"] = "bm=%d,bn=%d,bk=%d,wm=%d,wn=%d" % tile + f",pipe={pipe}"
+    try:
+        for _ in range(3):
+            pa.gemm(a, b, c, b_nk=b_nk)
+        torch.cuda.synchronize()
+        best = float("inf")
+        for _ in range(3):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(10):
+                pa.gemm(a, b, c, b_nk=b_nk)
+            e1.record()
+            torch.cuda.synchronize()
+            best = min(best, e0.elapsed_time(e1) / 10 * 1e3)
+        return best
+    finally:
+        os.environ.pop("ATTN_FORCE_GEMM", None)
+
+
+def calibrate_gemm(write: bool, out: str) -> None:
+    """Every valid GEMM tile kernel (both B layouts, every pipe), alone on a
+    CU (one tile per CU: M = 16 BM, N = 16 BN, K = 8192) and sharing CUs
+    (M = N = K = 4096)."""
+    import torch
+    from attn_inputs import random_bf16
+    desc = pa.DeviceDesc()
+    pa.lib.attn_query_device(ctypes.byref(desc))
+    table = {}
+    for shared in (False, True):
+        for b_nk in (False, True):
+            for ti, tile in enumerate(GEMM_TILES):
+                if shared:
+                    M, N, K = GEMM_SHAPE
+                else:
+                    side = int(round(desc.num_cus ** 0.5))
+                    M, N, K = side * tile[0], (desc.num_cus // side) * tile[1], 8192
+                a = random_bf16((M, K), 51).cuda()
+                b = random_bf16((N, K) if b_nk else (K, N), 52).cuda()
+                c = torch.empty((M, N), dtype=torch.float32, device="cuda")
+                for cand in pa.gemm_candidates(M, N, K, b_nk, device_footprint=True,
+                                               analytic_only=True):
+                    if (cand["BLOCK_M"], cand["BLOCK_N"], cand["BLOCK_K"], cand["WAVES_M"],
+                            cand["WAVES_N"]) != tile:
+                        continue
+                    if shared and cand["wg_per_cu"] < 2:
+                        continue  # cannot share a CU: only the alone setting applies
+                    t = time_gemm_tile(a, b, c, b_nk, tile, cand["PIPE"])
+                    f = t / cand["modeled_us"]
+                    table[(ti, b_nk, cand["PIPE"], shared)] = f
+                    print(f"gemm {'shared' if shared else 'alone '} b_nk={int(b_nk)} {tile} "
+                          f"pipe={cand['PIPE']} at {M}x{N}x{K}: measured {t:.1f} us, analytic "
+                          f"{cand['modeled_us']:.1f} us, factor {f:.3f}", flush=True)
+                del a, b, c
+    if write:
+        with open(GEMM_INC) as f:
+            head = f.read().split("static const float")[0]
+        rows = []
+        for i in range(len(GEMM_TILES)):
+            cells = ", ".join(
+                "{" + ", ".join("{" + ", ".join(f"{table.get((i, b_nk, p, sh), 0.0):.4f}f"
+                                                for sh in (False, True)) + "}"
+                                for p in range(3)) + "}" for b_nk in (False, True))
+            rows.append(f"    {{{cells}}},  // {GEMM_TILES[i]}")
+        with open(out, "w") as f:
+            f.write(head + "static const float kGemmPrimScale[9][2][3][2] = {\n" +
+                    "\n".join(rows) + "\n};\n")
+        print(f"wrote {out}")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--write", action="store_true", help="regenerate csrc/fwd_primitives.inc")
-    ap.add_argument("--out", default=INC, help="where --write puts the table")
+    ap.add_argument("--out", default=None, help="where --write puts the table")
+    ap.add_argument("--gemm", action="store_true", help="the GEMM tile kernels instead")
     a = ap.parse_args()
     import torch
     assert torch.cuda.is_available(), "characterisation needs a HIP device"
+    if a.gemm:
+        return calibrate_gemm(a.write, a.out or GEMM_INC)
+    a.out = a.out or INC
     from attn_inputs import random_bf16
     table = {}
     for d in (64, 128):

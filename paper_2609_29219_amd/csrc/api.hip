@@ -517,7 +517,13 @@ int attn__gemm_candidates(const attn_device_desc* desc, int M, int N, int K, int
     attn_device_desc local;
     GemmResFn res = nullptr;
     const bool have = attn_query_device(&local) == ATTN_OK && strcmp(local.arch, "gfx950") == 0;
-    if (have && (device_footprint || !desc)) res = gemm_resources;
+    // bit 0: the compiled kernels' real footprint; bit 1: the analytic model
+    // without the measured per-variant costs
+    if (have && ((device_footprint & 1) || !desc)) res = gemm_resources;
+    struct Scales {
+        explicit Scales(bool on) { use_fwd_primitive_costs(on); }
+        ~Scales() { use_fwd_primitive_costs(true); }
+    } scales(!(device_footprint & 2));
     if (!desc) desc = &local;
     if (buflen < 0 || (buflen > 0 && !buf)) return fail(ATTN_EINVAL, "bad output buffer");
     int rc = validate_gemm_dims(M, N, K, flags);

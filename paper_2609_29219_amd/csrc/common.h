@@ -145,7 +145,8 @@ inline long long fwd_workspace_bytes(const FwdPlan& p, long long rows) {
 int plan_fwd_all(const attn_device_desc& desc, int B, int H, int Sq, int Skv, int d, int causal,
                  FwdPlan* out, int cap, FwdResFn res = nullptr);
 bool fwd_resources(int d, int bn, int waves, int pipe, int causal, KernelRes* out);
-// Per-thread switch of the measured per-variant tile costs (on by default).
+// Per-thread switch of the measured per-variant tile costs, prefill and GEMM
+// (on by default).
 void use_fwd_primitive_costs(bool on);
 bool plan_decode(const attn_device_desc& desc, int B, int Hq, int Hkv, int Skv, int d,
                  int n_splits, DecodePlan* out);

@@ -29,6 +29,7 @@
 
 #include "common.h"
 #include "fwd_primitives.inc"
+#include "gemm_primitives.inc"
 
 namespace attn {
 
@@ -124,6 +125,14 @@ int fwd_vgprs(int d, int bn, int waves, int pipe) {
 // the analytic model alone (the calibration script does).
 static thread_local bool t_prim_scales = true;
 void use_fwd_primitive_costs(bool on) { t_prim_scales = on; }
+// GEMM tile kernels: index in kGemmTiles, B layout, pipe, and whether one
+// or several workgroups share a CU (a lone workgroup's waves cannot hide
+// each other's stalls, so its tiles cost more than the shared-CU model says).
+static double gemm_prim_scale(int tile, int b_nk, int pipe, bool shared_cu) {
+    if (!t_prim_scales || tile < 0 || tile >= 9 || pipe < 0 || pipe > 2) return 1.0;
+    const double f = kGemmPrimScale[tile][b_nk ? 1 : 0][pipe][shared_cu ? 1 : 0];
+    return f > 0.0 ? f : 1.0;
+}
 static double fwd_prim_scale(int d, int bn, int waves, int pipe, int causal) {
     const int di = d == 128 ? 1 : 0;
     const int bi = bn == 32 ? 0 : bn == 64 ? 1 : 2;
@@ -341,10 +350,12 @@ int gemm_lds_bytes(int bm, int bn, int bk, int b_nk, int pipe) {
 // written once) and L2 (A re-read once per tile column, B once per tile row).
 bool plan_gemm_fixed(const attn_device_desc& desc, int M, int N, int K, int b_nk, int bm, int bn,
                      int bk, int wm, int wn, int pipe, GemmPlan* out, GemmResFn res) {
-    bool known = false;
-    for (const GemmTile& t : kGemmTiles)
-        known |= t.bm == bm && t.bn == bn && t.bk == bk && t.wm == wm && t.wn == wn;
-    if (!known || pipe < 0 || pipe > 2) return false;
+    int tile_index = -1;
+    for (int i = 0; i < (int)(sizeof kGemmTiles / sizeof kGemmTiles[0]); ++i) {
+        const GemmTile& t = kGemmTiles[i];
+        if (t.bm == bm && t.bn == bn && t.bk == bk && t.wm == wm && t.wn == wn) tile_index = i;
+    }
+    if (tile_index < 0 || pipe < 0 || pipe > 2) return false;
     GemmPlan p;
     p.block_m = bm;
     p.block_n = bn;
@@ -383,15 +394,21 @@ bool plan_gemm_fixed(const attn_device_desc& desc, int M, int N, int K, int b_nk
     const double compute = 2.0 * bm * bn * bk / desc.mfma_bf16_flops_per_clk_cu;
     const double lds_bytes = waves * (double)(mb + nb) * 64.0 * bk + (double)(bm + bn) * bk * 2.0;
     const double lds = lds_bytes / desc.lds_bytes_per_clk_cu;
-    const double body1 = std::max(compute, lds);
+    // the compiled kernel's measured cost of a k-tile relative to this
+    // analytic body, alone on a CU or sharing it; load latency and bandwidth
+    // terms stay analytic
+    const double body1 =
+        std::max(compute, lds) * gemm_prim_scale(tile_index, b_nk, pipe, gr >= 2.0);
     const double body_g = gr * body1 + desc.tile_sync_cycles;
     // HBM share of a k-tile's bytes: the resident tiles of one XCD need each
     // of their distinct A and B panels once
     const double a_bytes = (double)bm * bk * 2.0, b_bytes = (double)bn * bk * 2.0;
     const double cus_xcd = (double)desc.num_cus / desc.num_xcds;
     const double xcd_tiles = std::max(1.0, std::min((double)p.grid / desc.num_xcds, cus_xcd * gr));
-    const double dm = std::min({(double)kGemmGroupM, (double)p.tiles_m, xcd_tiles});
-    const double dn = std::max(1.0, std::min((double)p.tiles_n, xcd_tiles / dm));
+    // the XCD's resident tiles run down groups of kGemmGroupM tile rows: they
+    // cover min(tiles_n, resident / GM) columns and the rows that fill them
+    const double dn = std::max(1.0, std::min((double)p.tiles_n, ceil(xcd_tiles / kGemmGroupM)));
+    const double dm = std::max(1.0, std::min((double)p.tiles_m, ceil(xcd_tiles / dn)));
     const double hbm_per_wg = std::min(a_bytes + b_bytes, (dm * a_bytes + dn * b_bytes) / xcd_tiles);
     const double f_hbm = hbm_per_wg / (a_bytes + b_bytes);
     const double hbm_lat = desc.hbm_latency_us * desc.clock_ghz * 1e3;  // cycles
