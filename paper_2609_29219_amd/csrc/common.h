@@ -81,10 +81,23 @@ constexpr int kDecodeUnroll = 8;
 constexpr int kGqaWaves = 4;      // waves of a grouped-query (matrix-core) decode workgroup
 constexpr int kGqaMinGroup = 4;   // smallest group served by the matrix-core decode
 
-// LDS footprint of a prefill workgroup: K tile [BN][D+8] and V tile
-// [BN][D+32] in bf16, one slot each (pipe 0) or two (pipe 1, 2, 3).
-constexpr int fwd_lds_bytes(int d, int bn, int pipe) {
-    return (pipe == 0 ? 1 : 2) * (bn * (d + 8) + bn * (d + 32)) * 2;
+// Output staging of the prefill epilogue: per wave, 32 rows of one 128-byte
+// piece each, padded to 144 bytes (it overlays the K/V slots).
+constexpr int kFwdStageRowBytes = 144;
+constexpr int kFwdStageWaveBytes = 32 * kFwdStageRowBytes;
+
+// LDS slots of the prefill kernel, in bf16 elements: K tile [BN][D+8] and V
+// tile [BN][D+32], each rounded up to whole 1 KiB pieces of the direct
+// global-to-LDS tile loads (512 elements).
+constexpr int fwd_k_slot_elems(int d, int bn) { return (bn * (d + 8) + 511) / 512 * 512; }
+constexpr int fwd_v_slot_elems(int d, int bn) { return (bn * (d + 32) + 511) / 512 * 512; }
+
+// LDS footprint of a prefill workgroup: one K and one V slot (pipe 0) or two
+// of each (pipe 1, 2, 3), and at least the waves' output staging.
+constexpr int fwd_lds_bytes(int d, int bn, int pipe, int waves) {
+    const int slots = (pipe == 0 ? 1 : 2) * (fwd_k_slot_elems(d, bn) + fwd_v_slot_elems(d, bn)) * 2;
+    const int stage = waves * kFwdStageWaveBytes;
+    return slots > stage ? slots : stage;
 }
 
 // Arguments of one prefill launch (every variant takes the same struct).

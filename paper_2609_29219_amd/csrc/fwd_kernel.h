@@ -90,8 +90,9 @@ template <int D, int BN>
 struct FwdLds {
     static constexpr int K_STRIDE = D + 8;   // bf16 per K row
     static constexpr int V_STRIDE = D + 32;  // bf16 per V row
-    static constexpr int K_TILE = BN * K_STRIDE;
-    static constexpr int V_TILE = BN * V_STRIDE;
+    // slot sizes rounded up to whole 1 KiB pieces of the direct tile loads
+    static constexpr int K_TILE = fwd_k_slot_elems(D, BN);
+    static constexpr int V_TILE = fwd_v_slot_elems(D, BN);
 };
 
 // LDS row of key j (0..31) inside a 32-key block; inverse of the permutation
@@ -132,7 +133,7 @@ constexpr int fwd_slots(int pipe) { return pipe == 0 ? 1 : 2; }
 // workgroups' LDS fits in one CU (or one 8-wave workgroup), else one.
 template <int D, int BN, int NW, int PIPE>
 constexpr int fwd_waves_per_eu() {
-    constexpr int lds = fwd_slots(PIPE) * (FwdLds<D, BN>::K_TILE + FwdLds<D, BN>::V_TILE) * 2;
+    constexpr int lds = fwd_lds_bytes(D, BN, PIPE, NW);
     constexpr int wgs = 163840 / lds;
     return (wgs * NW / 4) >= 2 ? 2 : 1;
 }
@@ -159,7 +160,8 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     constexpr int CH = (CHUNKS + NT - 1) / NT;
     constexpr int NSLOT = fwd_slots(PIPE);
 
-    __shared__ __attribute__((aligned(16))) uint16_t lds[NSLOT * (L::K_TILE + L::V_TILE)];
+    static_assert(fwd_lds_bytes(D, BN, PIPE, NW) >= NSLOT * (L::K_TILE + L::V_TILE) * 2, "");
+    __shared__ __attribute__((aligned(16))) uint16_t lds[fwd_lds_bytes(D, BN, PIPE, NW) / 2];
     uint16_t* const kslot0 = lds;
     uint16_t* const kslot1 = lds + (NSLOT - 1) * L::K_TILE;
     uint16_t* const vslot0 = lds + NSLOT * L::K_TILE;
@@ -314,48 +316,59 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     const uint32_t lds_base = lds_address(lds);
     // Piece p (0 <= p < KI + VI) goes to wave p % NW: K pieces first, then V.
     // off[j]: byte offset inside a tile of this lane's source chunk for the
-    // wave's j-th piece, -1 for none.
+    // wave's j-th piece.  Where a region ends inside its last piece, the lanes
+    // past its end fill the slot's padding (slots are whole pieces) with a
+    // copy of the region's last chunk, so whether a piece is issued is the
+    // wave-uniform piece < KI + VI and no lane is masked off.
+    static_assert(L::K_TILE * 2 >= KI * 1024 && L::V_TILE * 2 >= VI * 1024, "");
     int off[NJ];
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
         const int piece = wave + j * NW;
         const bool is_k = piece < KI;
-        const int i = is_k ? piece : piece - KI, pos = i * 64 + lane;
+        const int i = is_k ? piece : piece - KI;
+        const int pos = min(i * 64 + lane, (is_k ? KCH : VCH) - 1);
         const int st = is_k ? KST : VST;
         const int prow = pos / st, c = min(pos % st, DCH - 1);
         const int key = is_k ? (prow & ~31) | (16 * ((prow & 7) >> 2) + 4 * ((prow & 31) >> 3) +
                                               (prow & 3))
                              : prow;
-        const bool ok = piece < KI + VI && pos < (is_k ? KCH : VCH);
-        off[j] = ok ? (key * D + c * 8) * 2 : -1;
+        off[j] = (key * D + c * 8) * 2;
     }
-    // Issue this wave's pieces of K tile tk (into kdst) and/or V tile tv
-    // (into vdst); a negative tile index skips that operand.
-    auto dma = [&](int tk, uint16_t* kdst, int tv, uint16_t* vdst) __attribute__((always_inline)) {
+    // Issue this wave's pieces of K tile tk (into the K slot at element
+    // offset kdst of the LDS array) and/or V tile tv (into the V slot at
+    // vdst); a negative tile index skips that operand.  Slots are named by
+    // integer offsets: generic-pointer arithmetic on LDS addresses here made
+    // the backend emit an invalid null check.
+    auto dma = [&](int tk, int kdst, int tv, int vdst) __attribute__((always_inline)) {
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
             const int piece = wave + j * NW;
             if (piece >= KI + VI) continue;
             const bool is_k = piece < KI;
             const int t = is_k ? tk : tv;
-            if (t < 0 || off[j] < 0) continue;
+            if (t < 0) continue;
             const int key0 = t * BN;
             int o = off[j];
             if (key0 + BN > Skv)  // ragged tile: rows past the end re-read the last key
                 o = ((min(key0 + o / (2 * D), Skv - 1) - key0) * D) * 2 + o % (2 * D);
-            uint16_t* dst = is_k ? kdst + piece * 512 : vdst + (piece - KI) * 512;
+            const uint32_t dst = lds_base + (uint32_t)(is_k ? kdst + piece * 512
+                                                            : vdst + (piece - KI) * 512) * 2;
             if constexpr (PIPE == 0) {
                 // one slot: no read overlaps a load, the builtin's waits cost nothing
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                    is_k ? k_rsrc_b : v_rsrc_b, (__attribute__((address_space(3))) void*)dst,
-                    16, o, key0 * D * 2, 0, 0);
+                    is_k ? k_rsrc_b : v_rsrc_b,
+                    (__attribute__((address_space(3))) void*)(uintptr_t)dst, 16, o, key0 * D * 2,
+                    0, 0);
             } else {
-                lds_dma16(is_k ? k_rsrc : v_rsrc, lds_base + (uint32_t)(dst - lds) * 2, o,
-                          key0 * D * 2);
+                lds_dma16(is_k ? k_rsrc : v_rsrc, dst, o, key0 * D * 2);
             }
         }
     };
-    auto dma_k = [&](int t, uint16_t* dst) __attribute__((always_inline)) {
+    // element offsets of the slots in the LDS array
+    constexpr int KS0 = 0, KS1 = (NSLOT - 1) * L::K_TILE;
+    constexpr int VS0 = NSLOT * L::K_TILE, VS1 = VS0 + (NSLOT - 1) * L::V_TILE;
+    auto dma_k = [&](int t, int dst) __attribute__((always_inline)) {
         dma(t, dst, -1, dst);  // the V destination is unused
     };
 
@@ -595,7 +608,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     };
     if (PIPE == 0) {
         two_loops(0, [&](int t, auto mask_tag) {
-            dma(t, kslot0, t, vslot0);
+            dma(t, KS0, t, VS0);
             tile_barrier();
             if (wave_active(t)) {
                 f32x16 s[KB];
@@ -609,11 +622,11 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     } else if (PIPE == 1) {
         // tile t+1 streams into the other slot while tile t is computed from
         // LDS; one barrier per tile
-        dma(0, kslot0, 0, vslot0);
+        dma(0, KS0, 0, VS0);
         tile_barrier();
         two_loops(0, [&](int t, auto mask_tag) {
             const bool odd = t & 1;
-            if (t + 1 < n_tiles) dma(t + 1, odd ? kslot0 : kslot1, t + 1, odd ? vslot0 : vslot1);
+            if (t + 1 < n_tiles) dma(t + 1, odd ? KS0 : KS1, t + 1, odd ? VS0 : VS1);
             if (wave_active(t)) {
                 f32x16 s[KB];
                 bf16x8 pb[KB][2];
@@ -694,8 +707,8 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
         f32x16 sA[KB], sB[KB];
         bf16x8 pb[KB][2];
         float mx_next = -INFINITY;  // row max of the next tile's scores
-        dma(0, kslot0, 0, vslot0);
-        if (n_tiles > 1) dma_k(1, kslot1);
+        dma(0, KS0, 0, VS0);
+        if (n_tiles > 1) dma_k(1, KS1);
         tile_barrier();
         if (wave_active(0)) {
             scores(kslot0, sA);
@@ -710,8 +723,8 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
         // masking mode.
         auto iter = [&](int t, f32x16 (&s_cur)[KB], f32x16 (&s_nxt)[KB], auto mask_tag) __attribute__((always_inline)) {
             const bool odd = t & 1;
-            dma(t + 2 < n_tiles ? t + 2 : -1, odd ? kslot1 : kslot0,
-                t + 1 < n_tiles ? t + 1 : -1, odd ? vslot0 : vslot1);
+            dma(t + 2 < n_tiles ? t + 2 : -1, odd ? KS1 : KS0,
+                t + 1 < n_tiles ? t + 1 : -1, odd ? VS0 : VS1);
             const uint16_t* const k_next = odd ? kslot0 : kslot1;  // K_{t+1}
             const uint16_t* const v_cur = odd ? vslot1 : vslot0;   // V_t
             if (wave_active(t)) {
@@ -754,45 +767,90 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     // (not with the ping-pong schedule, which has no registers to spare)
     const bool partial = PIPE != 2 && kv_splits > 1;
     const float inv = partial ? 1.f : 1.f / l_row;
-    if (qrow < Sq) {
-        const long long row = (long long)bh * Sq + qrow;
-        const long long prow = row * kv_splits + split;  // == row when not split
-        if (args.out_bf16 && !partial) {
-            uint16_t* orow = static_cast<uint16_t*>(args.o) + row * D + 4 * hh;
-#pragma unroll
-            for (int cb = 0; cb < CB; ++cb)
-#pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    const bf16x2 lo = {(__bf16)(oacc[cb][4 * g] * inv),
-                                       (__bf16)(oacc[cb][4 * g + 1] * inv)};
-                    const bf16x2 hi = {(__bf16)(oacc[cb][4 * g + 2] * inv),
-                                       (__bf16)(oacc[cb][4 * g + 3] * inv)};
-                    const uint2 w = {__builtin_bit_cast(uint32_t, lo),
-                                     __builtin_bit_cast(uint32_t, hi)};
-                    *reinterpret_cast<uint2*>(orow + cb * 32 + 8 * g) = w;
-                }
-        } else {
-            float* const obase = partial ? args.ws_o : static_cast<float*>(args.o);
-            float* orow = obase + prow * D + 4 * hh;
-#pragma unroll
-            for (int cb = 0; cb < CB; ++cb)
-#pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    float4 val = {oacc[cb][4 * g] * inv, oacc[cb][4 * g + 1] * inv,
-                                  oacc[cb][4 * g + 2] * inv, oacc[cb][4 * g + 3] * inv};
-                    *reinterpret_cast<float4*>(orow + cb * 32 + 8 * g) = val;
-                }
-        }
-        if (hh == 0) {
-            float* const mdst = partial ? args.ws_m : args.lse;
-            if (mdst) mdst[prow] = partial ? m_i : (m_i + __builtin_log2f(l_row)) * kLn2;
-            if (partial) args.ws_l[prow] = l_row;
-        }
-    }
-    // Pipes 0, 1 and 3 end every tile with a barrier, after which no wave
-    // reads LDS, so the next q-tile may refill the slots at once; the
-    // ping-pong schedule reads V once more after its last barrier.
+    // The ping-pong schedule reads V once more after its last tile barrier.
     if (PIPE == 2) tile_barrier();
+    // Output rows leave through LDS.  A lane holds runs of 4 consecutive
+    // values of its row, so stores straight from registers touch 32 rows
+    // (32 cache lines) per instruction.  Instead each wave writes one 128-byte
+    // piece of each of its 32 rows (32 columns in fp32, 64 in bf16) into its
+    // own staging region and reads it back so that 8 lanes hold the piece of
+    // one row: each store instruction then writes 8 whole 128-byte lines.
+    // Every wave has passed the final tile barrier, so no wave reads the K/V
+    // slots any more and the staging regions may overlay them; within a wave
+    // the LDS writes and reads complete in order.
+    // The epilogue's kernel arguments are read here, behind an opaque zero
+    // offset, instead of being held in scalar registers through the tile
+    // loop, which is short of them.
+    int kz;
+    asm volatile("s_mov_b32 %0, 0" : "=s"(kz));
+    const FwdArgs& ea = *reinterpret_cast<const FwdArgs*>(reinterpret_cast<const char*>(&args) + kz);
+    const bool out16 = ea.out_bf16 && !partial;
+    // lane-derived addresses are recomputed here from an opaque copy of the
+    // lane index, rather than shared with values computed before the tile
+    // loop (which would then stay live, in registers, through the loop)
+    int elane = lane;
+    asm volatile("" : "+v"(elane));
+    const int el32 = elane & 31, ehh = elane >> 5;
+    uint8_t* const stage = reinterpret_cast<uint8_t*>(lds) + wave * kFwdStageWaveBytes;
+    constexpr int SROW = kFwdStageRowBytes;
+    const long long row0 = (long long)bh * Sq + q_wave0;  // this wave's first row
+    char* const obase = partial ? reinterpret_cast<char*>(ea.ws_o) : static_cast<char*>(ea.o);
+    const int row_bytes = out16 ? 2 * D : 4 * D;
+    auto emit = [&](int piece) __attribute__((always_inline)) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int r = (elane >> 3) + 8 * j;
+            const u32x4 w = *reinterpret_cast<const u32x4*>(stage + r * SROW + (elane & 7) * 16);
+            if (q_wave0 + r < Sq) {
+                const long long orow = partial ? (row0 + r) * kv_splits + split : row0 + r;
+                *reinterpret_cast<u32x4*>(obase + orow * row_bytes + piece * 128 + (elane & 7) * 16) = w;
+            }
+        }
+    };
+    if (out16) {
+        static_for<0, CB / 2>([&](auto pc) __attribute__((always_inline)) {
+            constexpr int piece = decltype(pc)::value;
+#pragma unroll
+            for (int half = 0; half < 2; ++half)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const f32x16& a = oacc[2 * piece + half];
+                    const bf16x2 lo = {(__bf16)(a[4 * g] * inv), (__bf16)(a[4 * g + 1] * inv)};
+                    const bf16x2 hi = {(__bf16)(a[4 * g + 2] * inv), (__bf16)(a[4 * g + 3] * inv)};
+                    *reinterpret_cast<uint32_t*>(stage + el32 * SROW + (half * 32 + 8 * g + 4 * ehh) * 2) =
+                        __builtin_bit_cast(uint32_t, lo);
+                    *reinterpret_cast<uint32_t*>(stage + el32 * SROW + (half * 32 + 8 * g + 4 * ehh) * 2 + 4) =
+                        __builtin_bit_cast(uint32_t, hi);
+                }
+            asm volatile("" ::: "memory");  // staging writes before the reads
+            emit(piece);
+            asm volatile("" ::: "memory");  // and the reads before the next piece's writes
+        });
+    } else {
+        static_for<0, CB>([&](auto pc) __attribute__((always_inline)) {
+            constexpr int cb = decltype(pc)::value;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const float4 val = {oacc[cb][4 * g] * inv, oacc[cb][4 * g + 1] * inv,
+                                    oacc[cb][4 * g + 2] * inv, oacc[cb][4 * g + 3] * inv};
+                *reinterpret_cast<u32x4*>(stage + el32 * SROW + (8 * g + 4 * ehh) * 4) =
+                    __builtin_bit_cast(u32x4, val);
+            }
+            asm volatile("" ::: "memory");
+            emit(cb);
+            asm volatile("" ::: "memory");
+        });
+    }
+    if (qrow < Sq && hh == 0) {
+        const long long prow = ((long long)bh * Sq + qrow) * kv_splits + split;  // row if unsplit
+        float* const mdst = partial ? ea.ws_m : ea.lse;
+        if (mdst) mdst[prow] = partial ? m_i : (m_i + __builtin_log2f(l_row)) * kLn2;
+        if (partial) ea.ws_l[prow] = l_row;
+    }
+    // Before the next q-tile's tile loads overwrite the staging regions, every
+    // wave has read its own back (the stores already hold the data, so only
+    // LDS operations are waited for, not the stores).
+    if (pass + 1 < n_pass) asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
     }  // pass
 }
 

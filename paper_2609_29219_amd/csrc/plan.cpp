@@ -152,7 +152,7 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
     p.pipe = pipe;
     p.causal = causal;
     p.block_m = 32 * waves;
-    p.lds_bytes = fwd_lds_bytes(d, bn, pipe);
+    p.lds_bytes = fwd_lds_bytes(d, bn, pipe, waves);
     p.vgprs = fwd_vgprs(d, bn, waves, pipe);
     // legality: capacities and primitive validity
     if (bn % 32 != 0 || d % 32 != 0) return false;
