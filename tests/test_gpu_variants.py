@@ -95,6 +95,33 @@ def test_fwd_bf16_output_is_the_rounded_fp32_output(pa, causal):
     compare(o16.float(), ref, "bf16 output")
 
 
+CAUSAL_SCHEDULES = [(32, 4, 0), (32, 8, 1), (64, 4, 1), (64, 8, 1), (32, 4, 3), (64, 8, 3),
+                    (128, 8, 0), (64, 8, 2)]
+
+
+@pytest.mark.parametrize("variant", CAUSAL_SCHEDULES, ids=[str(v) for v in CAUSAL_SCHEDULES])
+@pytest.mark.parametrize("d", [64, 128])
+def test_fwd_causal_rows_stored_early_every_schedule(pa, variant, d):
+    # A causal wave whose last key tile comes before its q-tile's last one
+    # stores its rows straight from registers while the other waves still
+    # compute.  Ragged Sq < Skv (the diagonal is offset), and several q-tiles
+    # so that workgroups run two passes; fp32 and bf16 rows and the LSE.
+    B, H, Sq, Skv = 1, 3, 600, 633
+    q, k, v = _qkv(B, H, H, Sq, Skv, d, 950 + d)
+    sc = float(np.float32(1.0 / math.sqrt(d)))
+    qd, kd, vd = q.to(DEV), k.to(DEV), v.to(DEV)
+    with forced_plan(*variant):
+        announce(f"attn_fwd_ex causal early stores {variant} d={d}")
+        o, lse = pa.attn_fwd(qd, kd, vd, scale=sc, causal=True, return_lse=True)
+        o16 = pa.attn_fwd(qd, kd, vd, scale=sc, causal=True, out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    ref, ref_lse = oracle.attn_gqa(q, k, v, B, H, H, Sq, Skv, d, sc, True)
+    compare(o, ref, f"causal {variant} d={d}")
+    compare(lse, ref_lse, f"causal {variant} d={d} lse", max_abs=LSE_MAX_ABS,
+            mean_abs=LSE_MEAN_ABS)
+    assert torch.equal(o16.cpu(), o.cpu().to(torch.bfloat16))
+
+
 def test_fwd_lse_special_cases(pa):
     # Q = 0: every allowed score is 0, lse = log(#allowed keys) (exact up to fp32)
     B, H, Sq, Skv, d = 1, 2, 100, 160, 64
