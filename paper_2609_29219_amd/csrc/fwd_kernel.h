@@ -509,7 +509,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
         constexpr int NS = HAS_S ? KB * KD : 0;  // MFMAs of S(t+1)
         constexpr int NPV = KB * 2 * CB;          // MFMAs of PV(t)
         constexpr int NM = NS + NPV;
-        constexpr int PF = CAUSAL ? 2 : 3;  // causal needs the registers
+        constexpr int PF = 3;
         constexpr int NPAIR = KB * 8;                    // pairs of probabilities per lane
         constexpr int EXP_SLOTS = HAS_S ? NS + NPV / 2 : 0;  // slots carrying exponentials
         constexpr int MAX0 = EXP_SLOTS + 1;              // first slot carrying the next max
