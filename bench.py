@@ -240,7 +240,8 @@ def main():
                      "traffic": profiled_traffic("prefill", wp.name),
                      "algorithmic_bytes": wp.hbm_bytes(),
                      "kernel": "fwd_kernel", "ms_per_launch": fwd_ms,
-                     "flops_per_launch": wp.flops()},
+                     "flops_per_launch": wp.flops(),
+                     "peak_from_device": device_peak(pa)},
         "decode": {"value": gbs, "unit": "GB/s", "ms_per_call": dec_ms,
                    "roofline": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS,
                                 "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS,
@@ -253,6 +254,16 @@ def main():
     if not a.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(wp, qp, kp, vp, a.cpu_seconds)
     print(json.dumps(rec), flush=True)
+
+
+def device_peak(pa) -> dict:
+    """The dense bf16 MFMA peak recomputed from the properties this device
+    reports (CUs x SIMDs x 1024 flop/clk x maximum clock), next to the
+    published figure the roofline uses."""
+    d = pa.query_device()
+    tflops = d["num_cus"] * d["simds_per_cu"] * 1024 * d["clock_ghz"] / 1e3
+    return {"value": tflops, "unit": "TFLOP/s", "cus": d["num_cus"],
+            "simds_per_cu": d["simds_per_cu"], "clock_ghz": d["clock_ghz"]}
 
 
 def gemm_leg(pa, dev, steps=20, warmup=10) -> dict:
