@@ -55,10 +55,10 @@ def source_hash(kind: str) -> str:
     return h.hexdigest()[:16]
 
 
-def profiled_traffic(kind: str, workload: str):
-    """HBM bytes per launch from the committed rocprofv3 summary, or None if the
-    kernel sources changed since the counters were taken."""
-    path = os.path.join(PROFILES, f"traffic_{workload}.txt")
+def _profile_fields(kind: str, name: str):
+    """key = value lines of a committed rocprofv3 summary, or None if it is
+    missing or the kernel sources changed since the counters were taken."""
+    path = os.path.join(PROFILES, name)
     if not os.path.exists(path):
         return None
     fields = {}
@@ -69,7 +69,20 @@ def profiled_traffic(kind: str, workload: str):
                 fields[k.strip()] = v.strip()
     if fields.get("source_sha256") != source_hash(kind):
         return None
-    return int(fields["traffic_bytes_per_launch"])
+    return fields
+
+
+def profiled_traffic(kind: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 summary (None if stale)."""
+    fields = _profile_fields(kind, f"traffic_{workload}.txt")
+    return None if fields is None else int(fields["traffic_bytes_per_launch"])
+
+
+def profiled_mfma_busy(workload: str):
+    """The prefill kernel's MFMA-busy share of SIMD cycles from the committed
+    counter summary (None if stale or absent)."""
+    fields = _profile_fields("prefill", f"mfma_{workload}.txt")
+    return None if fields is None else float(fields["mfma_busy_fraction"])
 
 
 def _args():
@@ -241,6 +254,7 @@ def main():
                      "algorithmic_bytes": wp.hbm_bytes(),
                      "kernel": "fwd_kernel", "ms_per_launch": fwd_ms,
                      "flops_per_launch": wp.flops(),
+                     "mfma_busy_fraction": profiled_mfma_busy(wp.name),
                      "peak_from_device": device_peak(pa)},
         "decode": {"value": gbs, "unit": "GB/s", "ms_per_call": dec_ms,
                    "roofline": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS,
