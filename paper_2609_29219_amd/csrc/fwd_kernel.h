@@ -217,21 +217,28 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
         return CAUSAL ? (pass == 0 ? n_qtiles - 1 - unit : unit) : unit;
     };
     // ---- Q tile into VGPRs, as the B operand (16 dims x 32 queries) ----------
+    // The loads are issued without touching the data, so nothing waits for
+    // them until the first MFMA that reads Q (the tile loads of the first K/V
+    // tiles, or the previous q-tile's epilogue, go on meanwhile).  A negative
+    // scale is applied by flipping the sign bits of Q (exact) at the start of
+    // the pass, only when it is negative.
     bf16x8 qf[KD];
     auto load_q = [&](int qt) __attribute__((always_inline)) {
         // rows past Sq read the last row (finite data; never stored)
         const int row = min(qt * BM + wave * 32 + l32, Sq - 1);
         const uint16_t* qp = Q + ((long long)bh * Sq + row) * D + hh * 8;
 #pragma unroll
-        for (int ks = 0; ks < KD; ++ks) {
-            u32x4 w = *reinterpret_cast<const u32x4*>(qp + ks * 16);
-            w ^= q_sign;  // exact negation for a negative scale
-            qf[ks] = __builtin_bit_cast(bf16x8, w);
-        }
+        for (int ks = 0; ks < KD; ++ks)
+            qf[ks] = *reinterpret_cast<const bf16x8*>(qp + ks * 16);
     };
     load_q(qt_of(0));
 
     for (int pass = 0; pass < n_pass; ++pass) {
+    if (q_sign) {
+#pragma unroll
+        for (int ks = 0; ks < KD; ++ks)
+            qf[ks] = __builtin_bit_cast(bf16x8, __builtin_bit_cast(u32x4, qf[ks]) ^ q_sign);
+    }
     const int qt = qt_of(pass);
     const int q_wave0 = qt * BM + wave * 32;  // first query row of this wave
     const int qrow = q_wave0 + l32;
@@ -796,14 +803,20 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     const long long row0 = (long long)bh * Sq + q_wave0;  // this wave's first row
     char* const obase = partial ? reinterpret_cast<char*>(ea.ws_o) : static_cast<char*>(ea.o);
     const int row_bytes = out16 ? 2 * D : 4 * D;
+    // (all four LDS reads first: the stores go through generic pointers,
+    // which the compiler would otherwise keep behind each read in turn)
     auto emit = [&](int piece) __attribute__((always_inline)) {
+        u32x4 w[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            w[j] = *reinterpret_cast<const u32x4*>(stage + ((elane >> 3) + 8 * j) * SROW +
+                                                   (elane & 7) * 16);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int r = (elane >> 3) + 8 * j;
-            const u32x4 w = *reinterpret_cast<const u32x4*>(stage + r * SROW + (elane & 7) * 16);
             if (q_wave0 + r < Sq) {
                 const long long orow = partial ? (row0 + r) * kv_splits + split : row0 + r;
-                *reinterpret_cast<u32x4*>(obase + orow * row_bytes + piece * 128 + (elane & 7) * 16) = w;
+                *reinterpret_cast<u32x4*>(obase + orow * row_bytes + piece * 128 + (elane & 7) * 16) = w[j];
             }
         }
     };
