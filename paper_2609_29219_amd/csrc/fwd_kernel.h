@@ -507,7 +507,8 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     // into pb) and, once S(t+1) is complete, the row max of tile t+1 (masked
     // in place first on MASK_NEXT tiles), which is returned.  Probabilities of
     // a 16-key step are produced before the PV MFMAs that consume them.  LDS
-    // operands are fetched PF MFMAs ahead, which also bounds their registers.
+    // operands come from a PF-entry ring, fetched PF - 1 MFMAs ahead (deeper
+    // rings measured no faster), which also bounds their registers.
     auto fused_tile = [&](const uint16_t* kl, const uint16_t* vl, const f32x16 (&s_cur)[KB],
                           f32x16 (&s_nxt)[KB], bf16x8 (&pb)[KB][2], int t, float m_ref,
                           auto has_s_tag, auto mask_tag) __attribute__((always_inline)) -> float {
@@ -516,7 +517,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
         constexpr int NS = HAS_S ? KB * KD : 0;  // MFMAs of S(t+1)
         constexpr int NPV = KB * 2 * CB;          // MFMAs of PV(t)
         constexpr int NM = NS + NPV;
-        constexpr int PF = 3;
+        constexpr int PF = 3;  // ring entries (fits 256 VGPRs also in the causal kernels)
         constexpr int NPAIR = KB * 8;                    // pairs of probabilities per lane
         constexpr int EXP_SLOTS = HAS_S ? NS + NPV / 2 : 0;  // slots carrying exponentials
         constexpr int MAX0 = EXP_SLOTS + 1;              // first slot carrying the next max
