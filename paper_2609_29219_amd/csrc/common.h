@@ -146,8 +146,10 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
                     int causal, int bn, int waves, int pipe, FwdPlan* out,
                     FwdResFn res = nullptr, int kv_splits = 1);
 // Key-split counts tried for non-causal prefill (each must leave every split
-// non-empty with a chunk that is a multiple of the tile width).
-constexpr int kFwdKvSplits[] = {1, 2, 3, 4, 6, 8, 12, 16, 24, 32};
+// non-empty with a chunk that is a multiple of the tile width, and the split
+// grid must stay within kFwdSplitRounds rounds of the CUs).
+constexpr int kFwdKvSplits[] = {1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48, 64, 96, 128, 192, 256};
+constexpr int kFwdSplitRounds = 4;
 // Bytes of the split-KV workspace: rows * splits * (d + 2) floats (the
 // partial outputs, then the maxima, then the sums).
 inline long long fwd_workspace_bytes(const FwdPlan& p, long long rows) {

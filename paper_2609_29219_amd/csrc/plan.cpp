@@ -189,6 +189,8 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
     // causal workgroups take q-tile pairs (n-1-u, u)
     p.grid = (long long)B * H * (causal ? (p.n_qtiles + 1) / 2 : (long long)p.n_qtiles * kv_splits);
     if (p.grid > 0x7fffffffLL) return false;
+    // splits fill the device; beyond a few rounds of it they only add partials
+    if (kv_splits > 1 && p.grid > (long long)kFwdSplitRounds * desc.num_cus) return false;
 
     const double mfma_cyc = 32768.0 / (desc.mfma_bf16_flops_per_clk_cu / simds);
     const double scores_per_lane = 32.0 * bn / desc.wave_size;

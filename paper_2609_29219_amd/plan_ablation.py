@@ -53,7 +53,7 @@ WORKLOADS = [
     ("b1_h2_s8192_d128", 1, 2, 8192, 8192, 128, False),
     ("b1_h32_q256_kv32768_d128", 1, 32, 256, 32768, 128, False),
 ]
-SPLITS = (1, 2, 3, 4, 6, 8, 12, 16, 24, 32)
+SPLITS = (1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48, 64, 96, 128, 192, 256)
 CALIBRATED = ("issue_cycles_per_score", "valu_mfma_overlap", "tile_sync_cycles",
               "tile_latency_cycles")
 

@@ -66,6 +66,7 @@ def dec(q=ALIGNED, k=ALIGNED, v=ALIGNED, o=ALIGNED, B=1, H=1, Skv=4, d=64, n=0):
     (dict(d=96), pa.ATTN_EUNSUPPORTED),
     (dict(d=256), pa.ATTN_EUNSUPPORTED),
     (dict(causal=1, Sq=5, Skv=4), pa.ATTN_EUNSUPPORTED),
+    (dict(Skv=0x7FFFFFFF // 256 + 1, d=128), pa.ATTN_EUNSUPPORTED),  # one head's K: 2 GiB
     (dict(scale=float("nan")), pa.ATTN_EINVAL),
     (dict(scale=float("inf")), pa.ATTN_EINVAL),
 ])
@@ -108,6 +109,8 @@ def test_gemm_rejects_on_host(kw, code):
 @pytest.mark.skipif(HAS_GPU, reason="checks the no-device path")
 def test_valid_call_without_device_is_a_hip_error_not_a_fallback():
     assert fwd() == pa.ATTN_EHIP
+    # the largest key range a head may have passes the host checks
+    assert fwd(Skv=0x7FFFFFFF // 256, d=128) == pa.ATTN_EHIP
     assert "device" in pa.last_error().lower() or "hip" in pa.last_error().lower()
     assert dec() == pa.ATTN_EHIP
     assert gemm() == pa.ATTN_EHIP

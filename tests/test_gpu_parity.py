@@ -212,6 +212,33 @@ def test_decode_special_cases(pa):
     np.testing.assert_allclose(o, v.double().numpy().mean(axis=2), atol=2e-6, rtol=0)
 
 
+def test_fwd_largest_key_range(pa):
+    # The largest K/V slab one head may have: the tile loads address a head's
+    # keys with 31-bit buffer offsets, so Skv * d * 2 bytes must stay below
+    # 2^31 (one key more is rejected on the host).  Ragged against every tile
+    # width; few queries, so the non-causal launch splits the key range; the
+    # causal one (bottom-right aligned) runs unsplit.  The outputs are small
+    # (softmax over 8M keys), so the relative error carries the check.
+    d = 128
+    Skv = 0x7FFFFFFF // (2 * d)  # 8,388,607 keys, 2^31 - 256 bytes per tensor
+    B, H, Sq = 1, 1, 40
+    q = random_bf16((B, H, Sq, d), 990)
+    k = random_bf16((B, H, Skv, d), 991)
+    v = random_bf16((B, H, Skv, d), 992)
+    qd, kd, vd = q.to(DEV), k.to(DEV), v.to(DEV)
+    rows = [0, 1, 17, Sq - 1]
+    scale = float(np.float32(1 / math.sqrt(d)))
+    for causal in (False, True):
+        announce(f"attn_fwd largest key range Skv={Skv} causal={causal} "
+                 f"plan {pa.get_plan(0, B, H, Sq, Skv, d, causal)}")
+        o = pa.attn_fwd(qd, kd, vd, scale=scale, causal=causal)
+        torch.cuda.synchronize()
+        flat = o.reshape(-1, d)
+        assert torch.isfinite(flat).all()
+        ref = oracle.attn_rows(q, k, v, rows, B, H, Sq, Skv, d, scale, causal)
+        compare(flat[rows], ref, f"Skv={Skv} causal={causal}", rel_fro=1e-2)
+
+
 # -------------------------------------------------- full-size workloads
 def _sample_rows(total_rows, Sq, rng, n=48):
     fixed = [0, 1, Sq - 1, Sq, total_rows - 1, total_rows // 2]

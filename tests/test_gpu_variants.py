@@ -283,6 +283,25 @@ def test_fwd_key_splits_one_key_in_last_split(pa):
     compare(o, oracle.attn(q, k, v, B, H, Sq, Skv, d, sc, False), "one-key split")
 
 
+@pytest.mark.parametrize("variant", [(64, 8, 3, 256), (128, 4, 1, 96), (32, 8, 1, 192)],
+                         ids=["64x8x3_256", "128x4x1_96", "32x8x1_192"])
+def test_fwd_many_key_splits(pa, variant):
+    # more splits than the 32 the combine saw before: one q-tile of a few
+    # queries against a long key range, the last split short
+    bn, waves, pipe, n = variant
+    B, H, Sq, d = 1, 2, 40, 128
+    Skv = n * 2 * bn - bn // 2  # chunk 2*bn, every split non-empty, the last half full
+    q, k, v = _qkv(B, H, H, Sq, Skv, d, 1350 + n)
+    sc = float(np.float32(1.0 / math.sqrt(d)))
+    announce(f"attn_fwd_ex many key splits {variant} Skv={Skv}")
+    with forced_split_plan(bn, waves, pipe, n):
+        o, lse = pa.attn_fwd(q.to(DEV), k.to(DEV), v.to(DEV), scale=sc, return_lse=True)
+    torch.cuda.synchronize()
+    ref, ref_lse = oracle.attn_gqa(q, k, v, B, H, H, Sq, Skv, d, sc, False)
+    compare(o, ref, f"{n} splits", rel_fro=1e-2)
+    compare(lse, ref_lse, f"{n} splits lse", max_abs=LSE_MAX_ABS, mean_abs=LSE_MEAN_ABS)
+
+
 def test_fwd_key_splits_chosen_by_the_planner(pa):
     # few heads and queries against many keys: the planner splits the keys
     B, H, Sq, Skv, d = 1, 2, 256, 12000, 128
