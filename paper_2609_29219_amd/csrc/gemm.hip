@@ -60,6 +60,7 @@ typedef __bf16 g_bf16x2 __attribute__((ext_vector_type(2)));
 typedef float g_f32x16 __attribute__((ext_vector_type(16)));
 typedef short g_s16x4 __attribute__((ext_vector_type(4)));
 typedef short g_s16x8 __attribute__((ext_vector_type(8)));
+typedef uint32_t g_u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kGroupM = 8;  // tile rows per group of the workgroup order
 
@@ -288,37 +289,66 @@ void gemm_kernel(const GemmArgs args) {
         }
     }
 
-    // ---- epilogue: lane (m, h) writes 4 consecutive columns per register group;
-    // one accumulator block at a time (the output type is decided outside the
-    // loops), so a wave holding 256 accumulators never needs them all in VGPRs
-    const int m = m0 + wm0 + l32;  // + 32 * mb
+    // ---- epilogue through LDS: a lane holds 4-column runs of one row of each
+    // 32x32 block, so storing from registers writes 16 (fp32) or 8 (bf16)
+    // bytes at each of 32 rows per instruction, which reach memory as partial
+    // lines.  Each wave instead writes one piece of its 32 rows -- a block's
+    // 32 columns in fp32 (128 bytes), two blocks' 64 columns in bf16 -- into
+    // its own staging region (rows padded to 144 bytes, overlaying the k-tile
+    // slots, which no wave reads after the last barrier), reads it back so
+    // that the lanes of one row hold its contiguous bytes, and stores whole
+    // lines.  The LDS writes and reads of a wave complete in order.
+    constexpr int SROW = 144;
+    static_assert(NSLOT * SLOT * 2 >= NW * 32 * SROW, "the staging regions fit the slots");
+    // lane-derived values recomputed from an opaque copy of the lane index
+    // (not shared with values held through the k-loop)
+    int elane = lane;
+    asm volatile("" : "+v"(elane));
+    const int el32 = elane & 31, ehh = elane >> 5;
+    uint8_t* const stage = reinterpret_cast<uint8_t*>(lds) + wave * 32 * SROW;
     auto store_all = [&](auto bf16_tag) __attribute__((always_inline)) {
         constexpr bool BF16 = decltype(bf16_tag)::value;
+        constexpr int ESZ = BF16 ? 2 : 4;
+        constexpr int NBP = (BF16 && NB % 2 == 0) ? 2 : 1;  // 32-column blocks per piece
+        constexpr int PB = 32 * NBP * ESZ;                  // bytes of a row's piece
+        constexpr int LPR = PB / 16;                        // lanes per row on read-back
+        constexpr int RPI = 64 / LPR;                       // rows per read instruction
+        char* const cbase = static_cast<char*>(args.c);
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
-            const int row = m + mb * 32;
 #pragma unroll
-            for (int nb = 0; nb < NB; ++nb) {
-                if (row < M) {
+            for (int np = 0; np < NB / NBP; ++np) {
+#pragma unroll
+                for (int q = 0; q < NBP; ++q) {
+                    const g_f32x16& c = acc[np * NBP + q][mb];
 #pragma unroll
                     for (int g = 0; g < 4; ++g) {
-                        const int col = n0 + wn0 + nb * 32 + 8 * g + 4 * hh;
-                        if (col >= N) continue;
-                        const g_f32x16& c = acc[nb][mb];
+                        uint8_t* dst = stage + el32 * SROW + (q * 32 + 8 * g + 4 * ehh) * ESZ;
                         if constexpr (BF16) {
                             const g_bf16x2 lo = {(__bf16)c[4 * g], (__bf16)c[4 * g + 1]};
                             const g_bf16x2 hi = {(__bf16)c[4 * g + 2], (__bf16)c[4 * g + 3]};
-                            const uint2 w = {__builtin_bit_cast(uint32_t, lo),
-                                             __builtin_bit_cast(uint32_t, hi)};
-                            *reinterpret_cast<uint2*>(static_cast<uint16_t*>(args.c) +
-                                                      (long long)row * N + col) = w;
+                            *reinterpret_cast<uint32_t*>(dst) = __builtin_bit_cast(uint32_t, lo);
+                            *reinterpret_cast<uint32_t*>(dst + 4) = __builtin_bit_cast(uint32_t, hi);
                         } else {
                             const float4 v = {c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]};
-                            *reinterpret_cast<float4*>(static_cast<float*>(args.c) +
-                                                       (long long)row * N + col) = v;
+                            *reinterpret_cast<g_u32x4*>(dst) = __builtin_bit_cast(g_u32x4, v);
                         }
                     }
                 }
+                asm volatile("" ::: "memory");  // staging writes before the reads
+                g_u32x4 w[32 / RPI];
+#pragma unroll
+                for (int j = 0; j < 32 / RPI; ++j)
+                    w[j] = *reinterpret_cast<const g_u32x4*>(stage + (elane / LPR + j * RPI) * SROW +
+                                                             (elane % LPR) * 16);
+                const int col = n0 + wn0 + np * NBP * 32 + (elane % LPR) * (16 / ESZ);
+#pragma unroll
+                for (int j = 0; j < 32 / RPI; ++j) {
+                    const int row = m0 + wm0 + mb * 32 + elane / LPR + j * RPI;
+                    if (row < M && col < N)
+                        *reinterpret_cast<g_u32x4*>(cbase + ((long long)row * N + col) * ESZ) = w[j];
+                }
+                asm volatile("" ::: "memory");  // and the reads before the next piece's writes
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
