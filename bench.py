@@ -152,12 +152,19 @@ def cpu_baseline(w, q, k, v, target_s: float) -> dict:
     t1 = run(1)
     n = int(max(1, min(heads, target_s / max(t1, 1e-6))))
     t = run(n) if n > 1 else t1
+    # when the whole workload takes less than the target, repeat whole passes
+    # over it until the target is reached (a steadier rate)
+    passes = 1
+    while n == heads and t < target_s and passes < 64:
+        t += run(n)
+        passes += 1
     sample = w.with_(B=1, H=n)
-    flops = sample.flops()
+    flops = sample.flops() * passes
+    reps = f" x {passes} passes" if passes > 1 else ""
     return {"value": flops / t / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
             "kind": "oracle",
-            "sample": f"{n} of {heads} (b,h) slabs of {w.name} ({flops / 1e9:.2f} GFLOP in "
-                      f"{t:.2f} s, fp64, {_cpu_model()})",
+            "sample": f"{n} of {heads} (b,h) slabs of {w.name}{reps} ({flops / 1e9:.2f} GFLOP "
+                      f"in {t:.2f} s, fp64, {_cpu_model()})",
             "seconds": t}
 
 
