@@ -310,7 +310,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     constexpr int KST = L::K_STRIDE / 8, VST = L::V_STRIDE / 8;  // per padded LDS row
     constexpr int KCH = BN * KST, VCH = BN * VST;                // positions per region
     constexpr int KI = (KCH + 63) / 64, VI = (VCH + 63) / 64;    // pieces per region
-    constexpr int NJ = (KI + VI + NW - 1) / NW;  // pieces per wave (K pieces, then V)
+    constexpr int NJK = (KI + NW - 1) / NW, NJV = (VI + NW - 1) / NW;  // pieces per wave
     const uint32_t slab_bytes = (uint32_t)Skv * D * 2;  // fits in 31 bits (checked by the host)
     const dma_rsrc_t k_rsrc = make_dma_rsrc(Kb, slab_bytes);
     const dma_rsrc_t v_rsrc = make_dma_rsrc(Vb, slab_bytes);
@@ -321,56 +321,77 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
         const_cast<uint16_t*>(Vb), 0, (int)slab_bytes, kRsrcFlags);
     // LDS byte address of the slots: the array's, plus element offsets
     const uint32_t lds_base = lds_address(lds);
-    // Piece p (0 <= p < KI + VI) goes to wave p % NW: K pieces first, then V.
-    // off[j]: byte offset inside a tile of this lane's source chunk for the
-    // wave's j-th piece.  Where a region ends inside its last piece, the lanes
-    // past its end fill the slot's padding (slots are whole pieces) with a
-    // copy of the region's last chunk, so whether a piece is issued is the
-    // wave-uniform piece < KI + VI and no lane is masked off.
+    // K piece p (0 <= p < KI) goes to wave p % NW, and so does V piece p
+    // (0 <= p < VI): the K/V choice of a piece is known at compile time and
+    // whether it exists is a scalar test on the wave index (only for a
+    // wave's last piece of each operand).  offk[j], offv[j]: byte offset
+    // inside a tile of this lane's source chunk for the wave's j-th K or V
+    // piece.  Where a region ends inside its last piece, the lanes past its
+    // end fill the slot's padding (slots are whole pieces) with a copy of the
+    // region's last chunk, so no lane is masked off.
     static_assert(L::K_TILE * 2 >= KI * 1024 && L::V_TILE * 2 >= VI * 1024, "");
-    int off[NJ];
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-        const int piece = wave + j * NW;
-        const bool is_k = piece < KI;
-        const int i = is_k ? piece : piece - KI;
-        const int pos = min(i * 64 + lane, (is_k ? KCH : VCH) - 1);
-        const int st = is_k ? KST : VST;
+    auto src_offset = [&](auto is_k_tag, int i) __attribute__((always_inline)) -> int {
+        constexpr bool IS_K = decltype(is_k_tag)::value;
+        const int pos = min(i * 64 + lane, (IS_K ? KCH : VCH) - 1);
+        constexpr int st = IS_K ? KST : VST;
         const int prow = pos / st, c = min(pos % st, DCH - 1);
-        const int key = is_k ? (prow & ~31) | (16 * ((prow & 7) >> 2) + 4 * ((prow & 31) >> 3) +
+        const int key = IS_K ? (prow & ~31) | (16 * ((prow & 7) >> 2) + 4 * ((prow & 31) >> 3) +
                                               (prow & 3))
                              : prow;
-        off[j] = (key * D + c * 8) * 2;
-    }
-    // Issue this wave's pieces of K tile tk (into the K slot at element
-    // offset kdst of the LDS array) and/or V tile tv (into the V slot at
-    // vdst); a negative tile index skips that operand.  Slots are named by
-    // integer offsets: generic-pointer arithmetic on LDS addresses here made
-    // the backend emit an invalid null check.
-    auto dma = [&](int tk, int kdst, int tv, int vdst) __attribute__((always_inline)) {
+        return (key * D + c * 8) * 2;
+    };
+    int offk[NJK], offv[NJV];
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) {
-            const int piece = wave + j * NW;
-            if (piece >= KI + VI) continue;
-            const bool is_k = piece < KI;
-            const int t = is_k ? tk : tv;
-            if (t < 0) continue;
-            const int key0 = t * BN;
-            int o = off[j];
-            if (key0 + BN > Skv)  // ragged tile: rows past the end re-read the last key
-                o = ((min(key0 + o / (2 * D), Skv - 1) - key0) * D) * 2 + o % (2 * D);
-            const uint32_t dst = lds_base + (uint32_t)(is_k ? kdst + piece * 512
-                                                            : vdst + (piece - KI) * 512) * 2;
-            if constexpr (PIPE == 0) {
-                // one slot: no read overlaps a load, the builtin's waits cost nothing
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                    is_k ? k_rsrc_b : v_rsrc_b,
-                    (__attribute__((address_space(3))) void*)(uintptr_t)dst, 16, o, key0 * D * 2,
-                    0, 0);
-            } else {
-                lds_dma16(is_k ? k_rsrc : v_rsrc, dst, o, key0 * D * 2);
+    for (int j = 0; j < NJK; ++j) offk[j] = src_offset(std::true_type{}, wave + j * NW);
+#pragma unroll
+    for (int j = 0; j < NJV; ++j) offv[j] = src_offset(std::false_type{}, wave + j * NW);
+    // The wave's pieces of one operand of tile t into the slot at element
+    // offset dst0 of the LDS array.  Slots are named by integer offsets:
+    // generic-pointer arithmetic on LDS addresses here made the backend emit
+    // an invalid null check.
+    auto dma_operand = [&](auto is_k_tag, int t, int dst0) __attribute__((always_inline)) {
+        constexpr bool IS_K = decltype(is_k_tag)::value;
+        constexpr int NI = IS_K ? KI : VI, NJO = IS_K ? NJK : NJV;
+        const int key0 = t * BN;
+        auto pieces = [&](auto ragged_tag) __attribute__((always_inline)) {
+#pragma unroll
+            for (int j = 0; j < NJO; ++j) {
+                const int i = wave + j * NW;
+                if ((j + 1) * NW > NI && i >= NI) continue;  // scalar; only the last piece
+                int o = IS_K ? offk[j] : offv[j];
+                if (ragged_tag)  // rows past the end re-read the last key
+                    o = ((min(key0 + o / (2 * D), Skv - 1) - key0) * D) * 2 + o % (2 * D);
+                const uint32_t dst = lds_base + (uint32_t)(dst0 + i * 512) * 2;
+                if constexpr (PIPE == 0) {
+                    // one slot: no read overlaps a load, the builtin's waits cost nothing
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                        IS_K ? k_rsrc_b : v_rsrc_b,
+                        (__attribute__((address_space(3))) void*)(uintptr_t)dst, 16, o,
+                        key0 * D * 2, 0, 0);
+                } else {
+                    lds_dma16(IS_K ? k_rsrc : v_rsrc, dst, o, key0 * D * 2);
+                }
             }
+        };
+        // the ragged tail tile in a branch of its own, so the common path
+        // issues its loads without any offset arithmetic (the causal kernels
+        // keep the compiler's select form: the second copy of the loads would
+        // push the software-pipelined one past its 256 registers)
+        if constexpr (CAUSAL) {
+            pieces(key0 + BN > Skv);
+        } else {
+            if (key0 + BN > Skv)
+                pieces(std::true_type{});
+            else
+                pieces(std::false_type{});
         }
+    };
+    // Issue this wave's pieces of K tile tk (into the K slot at kdst) and/or
+    // V tile tv (into the V slot at vdst); a negative tile index skips that
+    // operand.
+    auto dma = [&](int tk, int kdst, int tv, int vdst) __attribute__((always_inline)) {
+        if (tk >= 0) dma_operand(std::true_type{}, tk, kdst);
+        if (tv >= 0) dma_operand(std::false_type{}, tv, vdst);
     };
     // element offsets of the slots in the LDS array
     constexpr int KS0 = 0, KS1 = (NSLOT - 1) * L::K_TILE;
