@@ -111,9 +111,13 @@ def test_gemm_every_variant(pa, variant, pipe):
         announce(f"attn_gemm variant {variant} pipe={pipe} b_nk={b_nk}")
         with forced_gemm(*variant, pipe):
             c = pa.gemm(a.to(DEV), b.to(DEV), b_nk=b_nk)
+            c16 = pa.gemm(a.to(DEV), b.to(DEV), b_nk=b_nk, out_dtype=torch.bfloat16)
         torch.cuda.synchronize()
         want, absc = oracle.gemm(a, b, M, N, K, b_nk=b_nk, with_abs=True)
         _check(c, want, absc, K, f"variant {variant} pipe={pipe} b_nk={b_nk}")
+        # the bf16 epilogue (one or two 32-column blocks per staged piece) is
+        # the round-to-nearest-even of the fp32 one
+        assert torch.equal(c16.cpu(), c.cpu().to(torch.bfloat16)), f"bf16 {variant} pipe={pipe}" 
 
 
 def test_gemm_special_values(pa):
