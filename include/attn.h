@@ -42,7 +42,8 @@ extern "C" {
 
 #define ATTN_OK 0
 #define ATTN_EINVAL (-1)       /* null or misaligned pointer, a dim <= 0, bad buffer length */
-#define ATTN_EUNSUPPORTED (-2) /* d not in {64,128}, causal with Sq > Skv, device not gfx950 */
+#define ATTN_EUNSUPPORTED (-2) /* d not in {64,128}, causal with Sq > Skv, one head's K or V over \
+                                  2 GiB (prefill), device not gfx950 */
 #define ATTN_EHIP (-3)         /* HIP runtime or launch error (message in attn_last_error) */
 #define ATTN_ENOMEM (-4)       /* workspace allocation failed */
 
@@ -88,8 +89,10 @@ int attn_fwd(const void* q, const void* k, const void* v, float* o, int B, int H
  * to the per-stream workspace described under attn_decode, and a combine
  * kernel on the same stream writes o and lse.  Such a call may allocate or
  * grow that workspace (ATTN_ENOMEM on failure); the result equals the
- * unsplit one up to fp32 rounding.  attn_get_plan reports the choice
- * (KV_SPLITS, KV_CHUNK).
+ * unsplit one up to fp32 rounding.  Up to 256 splits, as long as the split
+ * grid stays within four rounds of the device's compute units (which bounds
+ * the workspace to rows * splits * (d + 2) * 4 bytes, at most ~136 MB).
+ * attn_get_plan reports the choice (KV_SPLITS, KV_CHUNK).
  * Errors as attn_fwd; EINVAL also for Hkv not dividing Hq, unknown flags or
  * a misaligned lse; EUNSUPPORTED if one head's K or V exceeds 2 GiB.
  */
