@@ -176,3 +176,35 @@ def test_gemm_rejects_before_launch(pa):
     c = torch.zeros((16, 16), dtype=torch.float32, device=DEV)
     rc = pa.lib.attn_gemm(a.data_ptr(), b.data_ptr(), c.data_ptr(), 16, 16, 16, 8)
     assert rc == pa.ATTN_EINVAL  # unknown flag
+
+
+def _sweep_shapes(n, seed=20261204):
+    """Seeded random shapes: M any size, N and K multiples of 8, log-uniform
+    (so every tile edge and sizes below one tile occur), at most 2^31
+    multiply-adds each for the oracle."""
+    g = np.random.default_rng(seed)
+    out = []
+    while len(out) < n:
+        M = int(round(np.exp(g.uniform(0, np.log(4000)))))
+        N = 8 * int(round(np.exp(g.uniform(0, np.log(500)))))
+        K = 8 * int(round(np.exp(g.uniform(0, np.log(800)))))
+        if M * N * K <= 1 << 31:
+            out.append((len(out), M, N, K, bool(g.integers(0, 2))))
+    return out
+
+
+SWEEP = _sweep_shapes(24)
+
+
+@pytest.mark.parametrize("case", SWEEP, ids=[f"{c[0]}-M{c[1]}-N{c[2]}-K{c[3]}-nk{int(c[4])}"
+                                              for c in SWEEP])
+def test_gemm_sweep(pa, case):
+    i, M, N, K, b_nk = case
+    a, b = _inputs(M, N, K, b_nk, 5000 + 2 * i)
+    announce(f"sweep attn_gemm {case}")
+    c = pa.gemm(a.to(DEV), b.to(DEV), b_nk=b_nk)
+    c16 = pa.gemm(a.to(DEV), b.to(DEV), b_nk=b_nk, out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    want, absc = oracle.gemm(a, b, M, N, K, b_nk=b_nk, with_abs=True)
+    _check(c, want, absc, K, f"sweep gemm {case}")
+    assert torch.equal(c16.cpu(), c.cpu().to(torch.bfloat16)), f"bf16 sweep {case}"
