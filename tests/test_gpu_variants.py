@@ -338,6 +338,35 @@ def test_fwd_key_splits_after_decode_share_the_workspace(pa):
     compare(dec, ref_d.reshape(B, H, d), "decode between")
 
 
+def test_two_streams_keep_separate_workspaces(pa):
+    # decode on one stream and split-key prefill on another, issued alternately
+    # so that both are in flight together: each stream's partials live in its
+    # own workspace, so neither result is disturbed by the other
+    B, H, Sq, Skv, d = 2, 4, 96, 3000, 128
+    q, k, v = _qkv(B, H, H, Sq, Skv, d, 1600)
+    qd = random_bf16((B, H, d), 1603)
+    sc = float(np.float32(1.0 / math.sqrt(d)))
+    qg, kg, vg, qdg = q.to(DEV), k.to(DEV), v.to(DEV), qd.to(DEV)
+    torch.cuda.synchronize()
+    s_dec, s_fwd = torch.cuda.Stream(), torch.cuda.Stream()
+    announce("decode and split prefill on two streams")
+    decs, fwds = [], []
+    with forced_split_plan(64, 4, 1, 8):
+        for _ in range(4):
+            with torch.cuda.stream(s_dec):
+                decs.append(pa.attn_decode(qdg, kg, vg, n_splits=12))
+            with torch.cuda.stream(s_fwd):
+                fwds.append(pa.attn_fwd(qg, kg, vg, scale=sc))
+    torch.cuda.synchronize()
+    for o in decs[1:]:
+        assert torch.equal(o.cpu(), decs[0].cpu())
+    for o in fwds[1:]:
+        assert torch.equal(o.cpu(), fwds[0].cpu())
+    compare(fwds[0], oracle.attn(q, k, v, B, H, Sq, Skv, d, sc, False), "split prefill stream")
+    ref_d = oracle.attn(qd.reshape(B, H, 1, d).contiguous(), k, v, B, H, 1, Skv, d, sc, False)
+    compare(decs[0], ref_d.reshape(B, H, d), "decode stream")
+
+
 def test_fwd_key_splits_rejected_for_causal(pa):
     q = torch.zeros((1, 1, 64, 64), dtype=torch.bfloat16, device=DEV)
     with forced_split_plan(64, 8, 1, 2):
