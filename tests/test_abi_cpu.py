@@ -123,6 +123,32 @@ def test_stream_round_trip():
     assert not pa.lib.attn_get_stream()
 
 
+def test_stream_and_last_error_are_per_thread():
+    # two threads set different streams and fail with different errors at the
+    # same time (ctypes releases the GIL in the calls); each sees its own
+    import threading
+    gate = threading.Barrier(2)
+    seen = {}
+
+    def worker(idx, stream, call):
+        assert pa.lib.attn_set_stream(ctypes.c_void_p(stream)) == pa.ATTN_OK
+        gate.wait()
+        rc = call()
+        gate.wait()
+        seen[idx] = (rc, pa.lib.attn_get_stream(), pa.last_error())
+        pa.lib.attn_set_stream(None)
+
+    calls = [lambda: fwd(q=None), lambda: fwd(d=96)]
+    ts = [threading.Thread(target=worker, args=(i, 0x1000 * (i + 1), calls[i])) for i in range(2)]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join()
+    assert seen[0][0] == pa.ATTN_EINVAL and seen[0][1] == 0x1000 and "null" in seen[0][2]
+    assert seen[1][0] == pa.ATTN_EUNSUPPORTED and seen[1][1] == 0x2000 and "96" in seen[1][2]
+    assert not pa.lib.attn_get_stream()  # this thread's stream is untouched
+
+
 @pytest.mark.skipif(HAS_GPU, reason="checks the no-device path")
 def test_query_device_without_device_gives_spec_values():
     desc = pa.DeviceDesc()
