@@ -167,6 +167,25 @@ def test_abi_rejects_before_launch(pa):
     assert (o == 7.0).all()
 
 
+@pytest.mark.parametrize("shape", [(0, 2, 8, 8), (1, 0, 8, 8), (1, 2, 0, 8), (1, 2, 8, 0)],
+                         ids=["B0", "H0", "Sq0", "Skv0"])
+def test_empty_inputs_rejected_through_the_binding(pa, shape):
+    # a zero-size batch, head set or sequence is an argument error (EINVAL),
+    # raised before any launch; decode likewise for B = 0, H = 0 or Skv = 0
+    B, H, Sq, Skv = shape
+    q = torch.zeros((B, H, Sq, 64), dtype=torch.bfloat16, device=DEV)
+    kv = torch.zeros((B, H, Skv, 64), dtype=torch.bfloat16, device=DEV)
+    announce(f"empty input {shape}")
+    with pytest.raises(pa.AttnError) as e:
+        pa.attn_fwd(q, kv, kv)
+    assert e.value.code == pa.ATTN_EINVAL
+    if Sq:
+        with pytest.raises(pa.AttnError) as e:
+            pa.attn_decode(q[:, :, 0].contiguous(), kv, kv)
+        assert e.value.code == pa.ATTN_EINVAL
+    torch.cuda.synchronize()
+
+
 # -------------------------------------------------------------------- decode
 def test_decode_small_and_split_invariance(pa):
     B, H, Skv, d = 2, 3, 1537, 128
