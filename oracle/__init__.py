@@ -15,7 +15,7 @@ What each function follows in the paper:
     the Evaluation section (matrix multiplication, softmax, value
     aggregation), written as the textbook definition.
   * ``attn_gqa`` -- the same definition with grouped-query heads and the
-    row log-sum-exp (variants the survey lists as next steps).
+    row log-sum-exp (variants beyond the paper's evaluation).
   * ``decode_split`` -- the Flash Decode decomposition in the HEG paragraph of
     the latency-modelling section (local softmax per chunk, gather partials,
     global softmax, final output).

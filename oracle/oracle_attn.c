@@ -18,7 +18,7 @@
  *   The max is subtracted before exp; that changes rounding only, not the
  *   exact value.
  *
- *   Variants (not in the paper's evaluation; the survey's next steps):
+ *   Variants (beyond the paper's evaluation):
  *   grouped-query heads -- query head h of Hq reads key/value head
  *   h / (Hq / Hkv) of Hkv -- and the log-sum-exp of each row's scores,
  *       lse_i = log sum_{j in A_i} exp(s_ij)  (natural log),
