@@ -171,8 +171,8 @@ def cpu_baseline(w, q, k, v, target_s: float) -> dict:
 def main():
     a = _args()
     if a.gpus != 1:
-        print(f"bench.py runs on exactly one GPU (asked for {a.gpus}); the path has no "
-              "multi-GPU form in this build", file=sys.stderr)
+        print(f"bench.py runs on exactly one GPU (asked for {a.gpus}); the attention path "
+              "has no multi-GPU form", file=sys.stderr)
         sys.exit(2)
     import torch
     import paper_2609_29219_amd as pa
