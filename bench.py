@@ -176,7 +176,7 @@ def main():
         sys.exit(2)
     import torch
     import paper_2609_29219_amd as pa
-    from attn_inputs import BY_NAME, CONFIGS
+    from attn_inputs import BY_NAME
 
     dev = "cuda:0"
     torch.cuda.set_device(0)
@@ -205,7 +205,7 @@ def main():
         print(json.dumps(rec), flush=True)
         return
 
-    wp, wd = CONFIGS[1], CONFIGS[3]
+    wp, wd = BY_NAME["prefill_b4_h16_s2048_d128_causal"], BY_NAME["decode_b16_h32_s8192_d128"]
     qp, kp, vp, qpd, kpd, vpd = _load_workload(wp, dev)
     _, _, _, qdd, kdd, vdd = _load_workload(wd, dev)
     op = torch.empty((wp.B, wp.H, wp.Sq, wp.d), dtype=torch.float32, device=dev)
