@@ -49,6 +49,8 @@ WORKLOADS = [
     ("b4_h16_s2048_d128_causal", 4, 16, 2048, 2048, 128, True),
     ("b4_h16_s2048_d64", 4, 16, 2048, 2048, 64, False),
     ("b8_h8_s1024_d128", 8, 8, 1024, 1024, 128, False),
+    # long causal at d = 64, where the VALU binds and another schedule wins
+    ("b4_h16_s8192_d64_causal", 4, 16, 8192, 8192, 64, True),
     # few heads / few queries against many keys: key splits fill the CUs
     ("b1_h2_s8192_d128", 1, 2, 8192, 8192, 128, False),
     ("b1_h32_q256_kv32768_d128", 1, 32, 256, 32768, 128, False),
