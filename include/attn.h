@@ -3,13 +3,13 @@
  * (gfx950), prefill (FlashAttention forward) and split-KV Flash-Decode.
  *
  * The operation.  The paper evaluates two attention kernels (Evaluation,
- * "Experimental Setup" and the Flash Attention / Flash Decode paragraphs):
- * Flash Attention, which combines a matrix multiplication, a softmax and a
- * value aggregation, and Flash Decode, where the query length is one and
- * the sequence (reduction) axis is split across cores, followed by a gather
- * of partial results, a global softmax and the final output (HEG paragraph
- * of the latency-modelling section).  Written out, for every batch b, head h
- * and query row i:
+ * Experimental Setup and the Flash Attention / Flash Decode paragraphs):
+ * Flash Attention -- query-key scores, a softmax over them, then the
+ * softmax-weighted sum of value rows -- and Flash Decode, its one-query
+ * form, whose key axis is cut into pieces handled in parallel and then
+ * merged: partial results are gathered, a softmax is taken across them and
+ * the output is formed (HEG paragraph of the latency-modelling section).
+ * Written out, for every batch b, head h and query row i:
  *     s_ij   = scale * sum_c q[b][h][i][c] * k[b][h][j][c]
  *     o[b][h][i][c] = sum_{j in A_i} exp(s_ij) v[b][h][j][c] / sum_{j in A_i} exp(s_ij)
  * with A_i = {0..Skv-1} (non-causal) or {j : j <= i + Skv - Sq} (causal,
@@ -111,10 +111,15 @@ int attn_fwd_ex(const void* q, const void* k, const void* v, void* o, float* lse
  *   rounding.
  * Workspace: B*H*n*(d+2)*4 bytes of device memory that the library owns and
  * keeps per stream, reused by every later call on that stream (decode and
- * split-key prefill; stream order serialises them) until the process ends.  A call that needs more than the
- * stream's current workspace drains that stream once, frees it and allocates
- * the next power of two; ATTN_ENOMEM if that allocation fails.  No other
- * call allocates or synchronises.
+ * split-key prefill; stream order serialises them) until the process ends.
+ * A call that needs more than the stream's current workspace allocates the
+ * next power of two in stream order (hipMallocAsync) and releases the old
+ * buffer in stream order (hipFreeAsync) behind the work already enqueued
+ * on that stream; it never waits for the device.  ATTN_ENOMEM if that
+ * allocation fails.  Host threads that share a stream are serialised from
+ * the moment a call takes the workspace until its kernels are enqueued, so
+ * a growth on one thread cannot release a buffer another thread's call is
+ * about to use.  No call synchronises.
  */
 int attn_decode(const void* q, const void* k, const void* v, float* o, int B, int H, int Skv,
                 int d, int n_splits);
@@ -205,9 +210,13 @@ int attn_measure_device(attn_device_desc* out);
 /*
  * Plan query: writes a one-line, human-readable plan -- the named tile
  * symbols (BLOCK_M, BLOCK_N, WAVES, PIPE, KV_SPLITS, KV_CHUNK for
- * ATTN_KIND_FWD; N_SPLITS, CHUNK, ... for ATTN_KIND_DECODE), the grid size, the modelled time in us and the
- * binding resource -- for the given problem into buf (NUL-terminated,
- * truncated to buflen).  Returns the full length of the line (excluding the
+ * ATTN_KIND_FWD; N_SPLITS, CHUNK, ... for ATTN_KIND_DECODE), the grid size,
+ * the modelled time in us and the binding resource -- for the given problem
+ * into buf (NUL-terminated, truncated to buflen).  This is the paper's
+ * reporting of solved schedule symbols under the names the program gave
+ * them (Symbolic MLIR subsection: symbols carry source-level labels, so the
+ * chosen values can be reported back by name), with the latency the model
+ * predicts (Eq. heg-optimization).  Returns the full length of the line (excluding the
  * NUL) or a negative ATTN_E* code.  Sq is ignored for decode.  desc may be
  * NULL (use attn_query_device()).  Host-only; launches nothing.
  */
@@ -218,8 +227,8 @@ int attn_get_plan_for(const attn_device_desc* desc, int kind, int B, int H, int 
 
 /*
  * Matrix multiplication C = A B, the paper's GEMM workload (Evaluation,
- * GEMM: "a regular dense-linear-algebra primitive with structured tiling
- * and high data reuse"), tiled by the same latency model.
+ * Experimental Setup and the GEMM paragraph: the dense, compute-bound case
+ * with heavy operand reuse), tiled by the same latency model.
  *   a: bf16 [M][K] row-major.
  *   b: bf16 [K][N] row-major, or with ATTN_GEMM_B_NK bf16 [N][K] row-major
  *      (c[m][n] = sum_k a[m][k] * b[n][k]).

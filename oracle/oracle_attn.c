@@ -7,9 +7,10 @@
  *
  * What it computes (plain definition, fp64, straight loops, no blocking):
  *   The paper evaluates Flash Attention and Flash Decode (Evaluation,
- *   "Experimental Setup": Flash Attention "combines matrix multiplication,
- *   softmax, and value aggregation"; Flash Decode streams the KV cache for a
- *   single query).  The paper never writes the formula; the textbook one is
+ *   Experimental Setup): scores from a product of queries and keys, a
+ *   softmax over the allowed keys, then a weighted sum of value rows; Flash
+ *   Decode is the same with one query per head, bound by reading the cached
+ *   keys and values.  The paper never writes the formula; the textbook one is
  *       s_ij = scale * sum_c q[i][c] k[j][c]        (matrix multiplication)
  *       P_ij = exp(s_ij) / sum_{j' in A_i} exp(s_ij') (softmax over allowed keys)
  *       o[i][c] = sum_{j in A_i} P_ij v[j][c]        (value aggregation)
@@ -305,8 +306,8 @@ int oracle_decode_split(const uint16_t* q, const uint16_t* k, const uint16_t* v,
 }
 
 /*
- * Matrix multiplication, the paper's third workload (Evaluation: GEMM, "a
- * regular dense-linear-algebra primitive"), as its plain definition in fp64
+ * Matrix multiplication, the paper's third workload (Evaluation, GEMM
+ * paragraph), as its plain definition in fp64
  * over bf16 inputs:
  *     c[m][n] = sum_{k < K} a[m][k] * b(k, n)
  * a: [M][K]; b: [K][N] with b(k, n) = b[k][n] (b_nk = 0), or [N][K] with

@@ -8,9 +8,13 @@
 #include <string.h>
 
 #include <algorithm>
+#include <atomic>
 #include <map>
+#include <memory>
 #include <mutex>
+#include <set>
 #include <string>
+#include <thread>
 #include <tuple>
 #include <vector>
 
@@ -101,24 +105,96 @@ int fail_hip(hipError_t e, const char* what) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
-// ---- per-device state --------------------------------------------------
-// The decode workspace is cached per stream and reused by every later call on
-// that stream (stream order serialises them).  Stream-ordered pool
-// allocation (hipMallocFromPoolAsync / hipFreeAsync) blocks the host until
-// the previous call's free has executed on this runtime, so it would turn
-// every decode call into a synchronisation.
-struct Workspace {
-    void* ptr = nullptr;
-    size_t bytes = 0;
+// ---- library-owned workspace ------------------------------------------
+// One buffer per stream, reused by every later call on that stream (stream
+// order serialises them) and grown to the next power of two when a call
+// needs more.  The stream's entry lock is held from the moment a call takes
+// the buffer until that call has enqueued its kernels: a call on another
+// host thread that grows the buffer therefore releases the old one only
+// after every kernel that uses it has been enqueued, and the release is
+// stream-ordered (it takes effect once the stream has passed those
+// kernels), so growth never waits for the device.  (hipFree synchronises
+// the whole device, so it is never called on this path.)  The map's own
+// lock guards only the map and is never held across an allocation.
+class WorkspaceMap {
+public:
+    // Stream-ordered allocation and release: HIP's, or a host-only double
+    // in the self-test.  Both return 0 or an ATTN_E* code.
+    struct Ops {
+        int (*alloc)(void* ctx, void* stream, size_t bytes, void** out);
+        int (*release)(void* ctx, void* stream, void* ptr);
+        void* ctx;
+    };
+    // On success *lk holds the stream's entry (keep it until the kernels
+    // that use *out are enqueued) and *out is its buffer of at least bytes.
+    int acquire(void* stream, size_t bytes, const Ops& ops, std::unique_lock<std::mutex>* lk,
+                void** out) {
+        Entry* e = nullptr;
+        {
+            std::lock_guard<std::mutex> g(mu_);
+            std::unique_ptr<Entry>& slot = entries_[stream];
+            if (!slot) slot.reset(new Entry);
+            e = slot.get();
+        }
+        std::unique_lock<std::mutex> l(e->mu);
+        if (e->bytes < bytes) {
+            size_t want = 4096;
+            while (want < bytes) want *= 2;
+            void* fresh = nullptr;
+            const int rc = ops.alloc(ops.ctx, stream, want, &fresh);
+            if (rc) return rc;
+            void* old = e->ptr;
+            e->ptr = fresh;
+            e->bytes = want;
+            // work already enqueued on the stream still reads the old buffer:
+            // released behind it, in stream order
+            if (old) {
+                const int rr = ops.release(ops.ctx, stream, old);
+                if (rr) return rr;
+            }
+        }
+        *out = e->ptr;
+        *lk = std::move(l);
+        return ATTN_OK;
+    }
+
+private:
+    struct Entry {
+        std::mutex mu;
+        void* ptr = nullptr;
+        size_t bytes = 0;
+    };
+    std::mutex mu_;
+    std::map<void*, std::unique_ptr<Entry>> entries_;
 };
+
+int hip_ws_alloc(void*, void* stream, size_t bytes, void** out) {
+    const hipError_t e = hipMallocAsync(out, bytes, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess || !*out) {
+        (void)hipGetLastError();
+        return fail(ATTN_ENOMEM, "workspace of %zu bytes: %s", bytes, hipGetErrorString(e));
+    }
+    return ATTN_OK;
+}
+
+int hip_ws_release(void*, void* stream, void* ptr) {
+    const hipError_t e = hipFreeAsync(ptr, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? ATTN_OK : fail_hip(e, "workspace release");
+}
+
+const WorkspaceMap::Ops kHipWorkspaceOps = {hip_ws_alloc, hip_ws_release, nullptr};
+
+// ---- per-device state --------------------------------------------------
+// Set up once per device, on the first call made with it current.
 struct DeviceState {
-    bool ready = false;
+    std::once_flag once;
+    hipError_t init_err = hipSuccess;
     bool is_gfx950 = false;
     attn_device_desc desc{};
-    std::map<hipStream_t, Workspace> ws;
+    WorkspaceMap ws;
 };
-std::mutex g_mu;
-std::map<int, DeviceState> g_devices;
+std::mutex g_mu;  // guards the maps below; never held across a HIP call
+std::map<int, DeviceState> g_devices;  // nodes never move
 std::map<std::tuple<int, int, int, int, int, int, int, int>, FwdPlan> g_fwd_cache;
 std::map<std::tuple<int, int, int, int, int, int, int>, DecodePlan> g_dec_cache;
 std::map<std::tuple<int, int, int, int, int>, GemmPlan> g_gemm_cache;
@@ -144,18 +220,20 @@ int device_state(DeviceState** out) {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return fail_hip(e, "hipGetDevice");
-    std::lock_guard<std::mutex> lk(g_mu);
-    DeviceState& st = g_devices[dev];
-    if (!st.ready) {
-        e = fill_desc(dev, &st.desc);
-        if (e != hipSuccess) return fail_hip(e, "hipGetDeviceProperties");
-        st.is_gfx950 = strcmp(st.desc.arch, "gfx950") == 0;
-        st.ready = true;
+    DeviceState* st = nullptr;
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        st = &g_devices[dev];
     }
-    if (!st.is_gfx950)
+    std::call_once(st->once, [&] {
+        st->init_err = fill_desc(dev, &st->desc);
+        st->is_gfx950 = st->init_err == hipSuccess && strcmp(st->desc.arch, "gfx950") == 0;
+    });
+    if (st->init_err != hipSuccess) return fail_hip(st->init_err, "hipGetDeviceProperties");
+    if (!st->is_gfx950)
         return fail(ATTN_EUNSUPPORTED, "device %d is %s; this library is built for gfx950", dev,
-                    st.desc.arch);
-    *out = &st;
+                    st->desc.arch);
+    *out = st;
     return ATTN_OK;
 }
 
@@ -171,32 +249,11 @@ bool forced_fwd(int* bn, int* waves, int* pipe, int* splits) {
 }
 
 // The per-stream workspace (decode partials, split-key prefill partials) of
-// at least bytes bytes.  Calls on one stream are serialised by the stream,
-// so they share one buffer.
-int stream_workspace(DeviceState* st, size_t bytes, void** out) {
-    std::lock_guard<std::mutex> lk(g_mu);
-    Workspace& w = st->ws[t_stream];
-    if (w.bytes < bytes) {
-        // grow to the next power of two; the old buffer may still be in use
-        // by work queued on this stream, so drain the stream first (rare)
-        size_t want = 4096;
-        while (want < bytes) want *= 2;
-        if (w.ptr) {
-            hipError_t e = hipStreamSynchronize(t_stream);
-            if (e == hipSuccess) e = hipFree(w.ptr);
-            if (e != hipSuccess) return fail_hip(e, "workspace release");
-            w = Workspace{};
-        }
-        hipError_t e = hipMalloc(&w.ptr, want);
-        if (e != hipSuccess || !w.ptr) {
-            (void)hipGetLastError();
-            w = Workspace{};
-            return fail(ATTN_ENOMEM, "workspace of %zu bytes: %s", want, hipGetErrorString(e));
-        }
-        w.bytes = want;
-    }
-    *out = w.ptr;
-    return ATTN_OK;
+// at least bytes bytes; *lk holds the stream's entry until the caller has
+// enqueued the kernels that use it.
+int stream_workspace(DeviceState* st, size_t bytes, std::unique_lock<std::mutex>* lk,
+                     void** out) {
+    return st->ws.acquire(t_stream, bytes, kHipWorkspaceOps, lk, out);
 }
 
 // Optional fixed GEMM tile for the block-size ablation only:
@@ -344,6 +401,65 @@ int attn__fwd_candidates(const attn_device_desc* desc, int B, int H, int Sq, int
     return len;
 }
 
+// Not part of the ABI: a host-only check of the workspace locking, with no
+// device.  threads host threads share simulated streams; for each of rounds
+// streams every thread makes calls that need a workspace twice as large as
+// its previous call (so most calls grow the buffer), and "enqueues" a job
+// naming the buffer it was given.  Allocation hands out fresh addresses and
+// release is enqueued on the simulated stream, like the HIP calls.  The
+// stream log is then replayed in order: a job that runs after its buffer's
+// release is a use after free.  hold_lock != 0 enqueues while holding the
+// entry lock (what the library does); hold_lock == 0 drops the lock first
+// and yields, the order in which a growth on another thread can release the
+// buffer before the job is enqueued.  Returns the number of such jobs.
+int attn__workspace_selftest(int threads, int rounds, int hold_lock) {
+    struct Sim {
+        std::mutex mu;
+        std::vector<std::pair<int, uintptr_t>> log;  // (0 job | 1 release, buffer)
+        std::atomic<uintptr_t> next{4096};
+    } sim;
+    auto alloc = [](void* ctx, void*, size_t bytes, void** out) -> int {
+        Sim* s = static_cast<Sim*>(ctx);
+        *out = reinterpret_cast<void*>(s->next.fetch_add((bytes + 4095) / 4096 * 4096));
+        return ATTN_OK;
+    };
+    auto release = [](void* ctx, void*, void* ptr) -> int {
+        Sim* s = static_cast<Sim*>(ctx);
+        std::lock_guard<std::mutex> g(s->mu);
+        s->log.emplace_back(1, reinterpret_cast<uintptr_t>(ptr));
+        return ATTN_OK;
+    };
+    const WorkspaceMap::Ops ops = {alloc, release, &sim};
+    WorkspaceMap map;
+    std::vector<std::thread> pool;
+    for (int t = 0; t < threads; ++t)
+        pool.emplace_back([&, t] {
+            for (int r = 0; r < rounds; ++r) {
+                void* stream = reinterpret_cast<void*>((uintptr_t)(r + 1) * 64);
+                for (int i = 0; i < 12; ++i) {
+                    std::unique_lock<std::mutex> lk;
+                    void* buf = nullptr;
+                    if (map.acquire(stream, ((size_t)2048 << i) + (size_t)t, ops, &lk, &buf))
+                        continue;
+                    if (!hold_lock) {
+                        lk.unlock();
+                        std::this_thread::yield();
+                    }
+                    std::lock_guard<std::mutex> g(sim.mu);
+                    sim.log.emplace_back(0, reinterpret_cast<uintptr_t>(buf));
+                }
+            }
+        });
+    for (auto& th : pool) th.join();
+    std::set<uintptr_t> released;
+    int bad = 0;
+    for (const auto& rec : sim.log) {
+        if (rec.first == 1) released.insert(rec.second);
+        else if (released.count(rec.second)) ++bad;
+    }
+    return bad;
+}
+
 int attn_get_plan(int kind, int B, int H, int Sq, int Skv, int d, int causal, int n_splits,
                   char* buf, int buflen) {
     return attn_get_plan_for(nullptr, kind, B, H, Sq, Skv, d, causal, n_splits, buf, buflen);
@@ -376,21 +492,27 @@ int attn_fwd_ex(const void* q, const void* k, const void* v, void* o, float* lse
                             fwd_resources_forced, fsplits))
             return fail(ATTN_EINVAL, "ATTN_FORCE_PLAN names an infeasible or unknown tile");
     } else {
-        std::lock_guard<std::mutex> lk(g_mu);
-        auto key = std::make_tuple(B, Hq, Sq, Skv, d, c, st->desc.num_cus, 0);
-        auto it = g_fwd_cache.find(key);
-        if (it != g_fwd_cache.end()) {
-            plan = it->second;
-        } else {
+        // looked up under the lock; planned (which queries the runtime for the
+        // compiled kernels' footprint) outside it
+        const auto key = std::make_tuple(B, Hq, Sq, Skv, d, c, st->desc.num_cus, 0);
+        bool hit = false;
+        {
+            std::lock_guard<std::mutex> lk(g_mu);
+            auto it = g_fwd_cache.find(key);
+            if ((hit = it != g_fwd_cache.end())) plan = it->second;
+        }
+        if (!hit) {
             if (!plan_fwd(st->desc, B, Hq, Sq, Skv, d, c, &plan, fwd_resources))
                 return fail(ATTN_EUNSUPPORTED, "no feasible prefill plan for this shape");
+            std::lock_guard<std::mutex> lk(g_mu);
             g_fwd_cache[key] = plan;
         }
     }
     const long long rows = (long long)B * Hq * Sq;
     void* ws = nullptr;
+    std::unique_lock<std::mutex> ws_lock;  // held until the kernels are enqueued
     if (plan.kv_splits > 1) {
-        rc = stream_workspace(st, (size_t)fwd_workspace_bytes(plan, rows), &ws);
+        rc = stream_workspace(st, (size_t)fwd_workspace_bytes(plan, rows), &ws_lock, &ws);
         if (rc) return rc;
     }
     hipError_t e = launch_fwd(plan, q, k, v, o, lse, Hq / Hkv, (flags & ATTN_OUT_BF16) ? 1 : 0,
@@ -408,15 +530,18 @@ int attn_fwd(const void* q, const void* k, const void* v, float* o, int B, int H
 // Plan of one decode call (cached per shape).
 static int decode_plan(DeviceState* st, int B, int Hq, int Hkv, int Skv, int d, int n_splits,
                        DecodePlan* plan) {
-    std::lock_guard<std::mutex> lk(g_mu);
-    auto key = std::make_tuple(B, Hq, Hkv, Skv, d, n_splits, st->desc.num_cus);
-    auto it = g_dec_cache.find(key);
-    if (it != g_dec_cache.end()) {
-        *plan = it->second;
-        return ATTN_OK;
+    const auto key = std::make_tuple(B, Hq, Hkv, Skv, d, n_splits, st->desc.num_cus);
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        auto it = g_dec_cache.find(key);
+        if (it != g_dec_cache.end()) {
+            *plan = it->second;
+            return ATTN_OK;
+        }
     }
     if (!plan_decode(st->desc, B, Hq, Hkv, Skv, d, n_splits, plan))
         return fail(ATTN_EUNSUPPORTED, "no feasible decode plan for this shape");
+    std::lock_guard<std::mutex> lk(g_mu);
     g_dec_cache[key] = *plan;
     return ATTN_OK;
 }
@@ -459,12 +584,13 @@ int attn_decode_ex(const void* q, const void* k, const void* v, float* o, float*
     if (rc) return rc;
     const size_t ws_bytes = (size_t)B * Hq * plan.n_splits * (d + 2) * sizeof(float);
     void* ws = workspace;
+    std::unique_lock<std::mutex> ws_lock;  // held until the kernels are enqueued
     if (ws) {
         if (workspace_bytes < ws_bytes)
             return fail(ATTN_EINVAL, "workspace of %zu bytes, %zu needed", workspace_bytes,
                         ws_bytes);
     } else {
-        rc = stream_workspace(st, ws_bytes, &ws);
+        rc = stream_workspace(st, ws_bytes, &ws_lock, &ws);
         if (rc) return rc;
     }
     const float scale = (float)(1.0 / sqrt((double)d));
@@ -563,14 +689,17 @@ int attn_gemm(const void* a, const void* b, void* c, int M, int N, int K, int fl
                              gemm_resources_forced))
             return fail(ATTN_EINVAL, "ATTN_FORCE_GEMM names an infeasible or unknown tile");
     } else {
-        std::lock_guard<std::mutex> lk(g_mu);
-        auto key = std::make_tuple(M, N, K, b_nk, st->desc.num_cus);
-        auto it = g_gemm_cache.find(key);
-        if (it != g_gemm_cache.end()) {
-            plan = it->second;
-        } else {
+        const auto key = std::make_tuple(M, N, K, b_nk, st->desc.num_cus);
+        bool hit = false;
+        {
+            std::lock_guard<std::mutex> lk(g_mu);
+            auto it = g_gemm_cache.find(key);
+            if ((hit = it != g_gemm_cache.end())) plan = it->second;
+        }
+        if (!hit) {
             if (!plan_gemm(st->desc, M, N, K, b_nk, &plan, gemm_resources))
                 return fail(ATTN_EUNSUPPORTED, "no feasible GEMM plan for this shape");
+            std::lock_guard<std::mutex> lk(g_mu);
             g_gemm_cache[key] = plan;
         }
     }

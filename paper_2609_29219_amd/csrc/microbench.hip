@@ -1,7 +1,7 @@
 // Microbenchmarks that measure the performance properties of the device
 // description (the paper's architecture-description section: structural
 // properties come from the specification, performance properties from
-// isolated microbenchmarks, collected once per architecture and reused for
+// isolated microbenchmarks, measured a single time per architecture and used for
 // every shape).  Each kernel saturates one primitive on every CU:
 //   mfma  -- independent v_mfma_f32_32x32x16_bf16 chains, 4 waves per CU
 //   valu  -- independent fp32 FMA chains

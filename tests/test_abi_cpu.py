@@ -162,3 +162,18 @@ def test_query_device_without_device_gives_spec_values():
 def test_null_descriptor_rejected():
     assert pa.lib.attn_query_device(None) == pa.ATTN_EINVAL
     assert pa.lib.attn_measure_device(None) == pa.ATTN_EINVAL
+
+
+def test_workspace_growth_cannot_release_a_buffer_before_its_users_are_enqueued():
+    # Host-only check of the library's workspace locking (no device): eight
+    # threads share simulated streams and grow the workspace on most calls;
+    # replaying each stream in order, no job may run after the release of the
+    # buffer it was given.  The same replay with the entry lock dropped
+    # before enqueueing (the order the library avoids) finds such jobs, so
+    # the check can see the race it guards against.
+    f = pa.lib.attn__workspace_selftest
+    f.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int]
+    f.restype = ctypes.c_int
+    for _ in range(5):
+        assert f(8, 200, 1) == 0
+    assert any(f(8, 200, 0) > 0 for _ in range(20))

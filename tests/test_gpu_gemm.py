@@ -167,6 +167,31 @@ def test_gemm_large_sampled_rows(pa, shape):
     _check(c.cpu()[torch.from_numpy(rows)], want, absc, K, f"large {shape}")
 
 
+@pytest.mark.timeout(900)
+def test_gemm_bench_shape_every_element(pa):
+    # the benchmark's GEMM (8192^3, B stored [K][N], fp32 C, the same seeded
+    # operands and the planner's tile), every output element against the
+    # oracle, on an output filled with NaN first.  The oracle reads B^T
+    # through its [N][K] path (the same sums; its inner loop then runs along
+    # contiguous rows).
+    M = N = K = 8192
+    a, b = random_bf16((M, K), 31), random_bf16((K, N), 32)
+    announce(f"attn_gemm {M}x{N}x{K} every element, plan {pa.gemm_plan(M, N, K)}")
+    c = torch.full((M, N), float("nan"), dtype=torch.float32, device=DEV)
+    pa.gemm(a.to(DEV), b.to(DEV), c)
+    torch.cuda.synchronize()
+    got = c.cpu()
+    del c
+    announce(f"oracle GEMM {M}x{N}x{K} in fp64 on {oracle.num_threads()} threads")
+    want, absc = oracle.gemm(a, b.t().contiguous(), M, N, K, b_nk=True, with_abs=True)
+    _check(got, want, absc, K, "gemm 8192^3")
+    err = np.abs(got.double().numpy() - want)
+    print(f"[full-size parity] gemm_m8192_n8192_k8192: max_abs={err.max():.3e} "
+          f"mean_abs={err.mean():.3e} max_err_over_bound="
+          f"{float(np.max(err / (2.0 * (K / 16 + 16) * 2.0 ** -24 * absc + 1e-30))):.3f}",
+          flush=True)
+
+
 def test_gemm_rejects_before_launch(pa):
     a = torch.zeros((16, 12), dtype=torch.bfloat16, device=DEV)
     b = torch.zeros((12, 16), dtype=torch.bfloat16, device=DEV)

@@ -1,11 +1,12 @@
 """GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
 
-All inputs are seeded and synthetic (attn_inputs).  Small shapes compare
-every output element with the oracle; the full-size workloads compare
-sampled rows that the oracle computes one by one, in the same launch
-configuration the benchmark times.  Tolerances: max-abs 2e-2 and mean-abs
-2e-3 over the compared elements (bf16 inputs, fp32 accumulation); special
-cases with exact answers are checked much tighter.
+All inputs are seeded and synthetic (attn_inputs).  Every test compares
+every output element with the oracle, the five workloads included (at full
+size, in the launch configuration the benchmark times, on NaN-filled
+outputs); only the largest key range a head may have (8M keys) compares
+sampled rows.  Tolerances: max-abs 2e-2 and mean-abs 2e-3 over all output
+elements (bf16 inputs, fp32 accumulation); special cases with exact answers
+are checked much tighter.
 """
 from __future__ import annotations
 
@@ -45,15 +46,21 @@ def _fwd_case(pa, B, H, Sq, Skv, d, causal, seed, scale=None, **tol):
     return compare(o, ref, f"fwd {B,H,Sq,Skv,d,causal}", **tol)
 
 
+def _report(name, stats):
+    print(f"[full-size parity] {name}: max_abs={stats['max_abs']:.3e} "
+          f"mean_abs={stats['mean_abs']:.3e} rel_fro={stats['rel_fro']:.3e}", flush=True)
+
+
 # ------------------------------------------------------------ small shapes
 def test_config_single_head(pa):
     w = CONFIGS[0]
     q, k, v = make_inputs(w)
     announce(f"attn_fwd {w.name}")
-    o = pa.attn_fwd(q.to(DEV), k.to(DEV), v.to(DEV), scale=w.scale, causal=w.causal)
+    o = torch.full((w.B, w.H, w.Sq, w.d), float("nan"), dtype=torch.float32, device=DEV)
+    pa.attn_fwd(q.to(DEV), k.to(DEV), v.to(DEV), o=o, scale=w.scale, causal=w.causal)
     torch.cuda.synchronize()
     ref = oracle.attn(q, k, v, w.B, w.H, w.Sq, w.Skv, w.d, w.scale, w.causal)
-    compare(o, ref, w.name, rel_fro=1e-2)
+    _report(w.name, compare(o, ref, w.name, rel_fro=1e-2))
 
 
 SMALL = [  # B, H, Sq, Skv, d, causal
@@ -259,36 +266,40 @@ def test_fwd_largest_key_range(pa):
 
 
 # -------------------------------------------------- full-size workloads
-def _sample_rows(total_rows, Sq, rng, n=48):
-    fixed = [0, 1, Sq - 1, Sq, total_rows - 1, total_rows // 2]
-    rnd = rng.choice(total_rows, size=n, replace=False).tolist()
-    return sorted(set(r for r in fixed + rnd if 0 <= r < total_rows))
-
-
+# Every output element of the four full-size workloads against the fp64
+# oracle, in the launch configuration the benchmark times (the planner's
+# choice), on outputs filled with NaN first, so an element the kernels never
+# write fails.  Max-abs and mean-abs are taken over all B*H*Sq*d elements.
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("idx", [1, 2], ids=[CONFIGS[1].name, CONFIGS[2].name])
-def test_fwd_full_size_sampled(pa, idx):
+def test_fwd_full_size_every_element(pa, idx):
     w = CONFIGS[idx]
     q, k, v = make_inputs(w)
-    announce(f"attn_fwd full size {w.name}")
-    o = pa.attn_fwd(q.to(DEV), k.to(DEV), v.to(DEV), scale=w.scale, causal=w.causal)
+    announce(f"attn_fwd full size {w.name} plan "
+             f"{pa.get_plan(pa.KIND_FWD, w.B, w.H, w.Sq, w.Skv, w.d, w.causal)}")
+    o = torch.full((w.B, w.H, w.Sq, w.d), float("nan"), dtype=torch.float32, device=DEV)
+    pa.attn_fwd(q.to(DEV), k.to(DEV), v.to(DEV), o=o, scale=w.scale, causal=w.causal)
     torch.cuda.synchronize()
-    flat = o.reshape(-1, w.d)
-    assert torch.isfinite(flat).all()
-    rows = _sample_rows(w.B * w.H * w.Sq, w.Sq, np.random.default_rng(w.seed))
-    ref = oracle.attn_rows(q, k, v, rows, w.B, w.H, w.Sq, w.Skv, w.d, w.scale, w.causal)
-    compare(flat[rows], ref, w.name, rel_fro=1e-2)
+    got = o.cpu()
+    del o
+    announce(f"oracle {w.name} ({w.flops() / 1e9:.0f} GFLOP in fp64 on "
+             f"{oracle.num_threads()} threads)")
+    ref = oracle.attn(q, k, v, w.B, w.H, w.Sq, w.Skv, w.d, w.scale, w.causal)
+    _report(w.name, compare(got, ref, w.name, rel_fro=1e-2))
 
 
+@pytest.mark.timeout(600)
 @pytest.mark.parametrize("idx", [3, 4], ids=[CONFIGS[3].name, CONFIGS[4].name])
-def test_decode_full_size_sampled(pa, idx):
+def test_decode_full_size_every_element(pa, idx):
     w = CONFIGS[idx]
     q, k, v = make_inputs(w)
-    announce(f"attn_decode full size {w.name}")
-    o = pa.attn_decode(q.to(DEV), k.to(DEV), v.to(DEV), n_splits=0)
+    announce(f"attn_decode full size {w.name} plan "
+             f"{pa.get_plan(pa.KIND_DECODE, w.B, w.H, 1, w.Skv, w.d)}")
+    o = torch.full((w.B, w.H, w.d), float("nan"), dtype=torch.float32, device=DEV)
+    pa.attn_decode(q.to(DEV), k.to(DEV), v.to(DEV), o=o, n_splits=0)
     torch.cuda.synchronize()
-    assert torch.isfinite(o).all()
-    flat = o.reshape(-1, w.d)
-    rows = _sample_rows(w.B * w.H, 1, np.random.default_rng(w.seed), n=min(24, w.B * w.H - 4))
-    ref = oracle.attn_rows(q.reshape(w.B, w.H, 1, w.d), k, v, rows, w.B, w.H, 1, w.Skv, w.d,
-                           w.scale, False)
-    compare(flat[rows], ref, w.name, rel_fro=1e-2)
+    got = o.cpu()
+    announce(f"oracle {w.name}")
+    ref = oracle.attn(q.reshape(w.B, w.H, 1, w.d), k, v, w.B, w.H, 1, w.Skv, w.d, w.scale,
+                      False)
+    _report(w.name, compare(got, ref.reshape(w.B, w.H, w.d), w.name, rel_fro=1e-2))
