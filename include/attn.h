@@ -146,6 +146,31 @@ int attn_decode_ex(const void* q, const void* k, const void* v, float* o, float*
                    int Hq, int Hkv, int Skv, int d, int n_splits, void* workspace,
                    size_t workspace_bytes);
 
+/*
+ * Decode that allocates nothing, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc).  Same operation, arguments, plan and kernels as
+ * attn_decode_ex with workspace = NULL, and the same result bit for bit;
+ * the split partials go to a static device array of
+ * ATTN_NOALLOC_SCRATCH_BYTES that the library holds on every device it runs
+ * on until the process ends (its address is looked up once per device, on
+ * the first call made with that device current).
+ *   Limit: B * Hq * n * (d + 2) * 4 bytes must fit in the scratch (n = the
+ *   planned or requested split count, as attn_decode_workspace_bytes
+ *   reports); a larger call fails with ATTN_ENOMEM before any launch.
+ *   Concurrency: every call on one device shares that device's scratch, and
+ *   it keeps the last call's partials.  Calls ordered on one stream are
+ *   safe; calls that can overlap on one device (different streams, or host
+ *   threads with no ordering between their streams) race on it.
+ * Calls no allocation routine (no hipMalloc, hipFree or stream-ordered
+ * allocation); asynchronous on the thread's stream; errors as
+ * attn_decode_ex, plus ATTN_ENOMEM for a call over the limit and ATTN_EHIP
+ * if the scratch address cannot be obtained.
+ */
+#define ATTN_NOALLOC_SCRATCH_BYTES (16u << 20)
+int attn_decode_noalloc(const void* q, const void* k, const void* v, float* o, float* lse, int B,
+                        int Hq, int Hkv, int Skv, int d, int n_splits);
+
 /* Bytes of decode workspace attn_decode_ex needs for this problem (plans
  * the call; needs the device), or a negative ATTN_E* code. */
 long long attn_decode_workspace_bytes(int B, int Hq, int Hkv, int Skv, int d, int n_splits);

@@ -33,7 +33,8 @@ ATTN_GEMM_B_NK = 2
 EXPORTED = ("attn_fwd", "attn_decode", "attn_fwd_ex", "attn_decode_ex",
             "attn_decode_workspace_bytes", "attn_set_stream", "attn_get_stream",
             "attn_last_error", "attn_query_device", "attn_measure_device", "attn_get_plan",
-            "attn_get_plan_for", "attn_gemm", "attn_gemm_plan")
+            "attn_get_plan_for", "attn_gemm", "attn_gemm_plan", "attn_decode_noalloc")
+NOALLOC_SCRATCH_BYTES = 16 << 20  # ATTN_NOALLOC_SCRATCH_BYTES
 
 
 class AttnError(RuntimeError):
@@ -92,6 +93,7 @@ def _load() -> ctypes.CDLL:
     lib.attn_fwd_ex.argtypes = [vp, vp, vp, vp, vp, ci, ci, ci, ci, ci, ci, cf, ci, ci]
     lib.attn_decode_ex.argtypes = [vp, vp, vp, vp, vp, ci, ci, ci, ci, ci, ci, vp,
                                    ctypes.c_size_t]
+    lib.attn_decode_noalloc.argtypes = [vp, vp, vp, vp, vp, ci, ci, ci, ci, ci, ci]
     lib.attn_decode_workspace_bytes.argtypes = [ci, ci, ci, ci, ci, ci]
     lib.attn_decode_workspace_bytes.restype = ctypes.c_longlong
     lib.attn_set_stream.argtypes = [vp]
@@ -112,6 +114,7 @@ def _load() -> ctypes.CDLL:
     lib.attn__gemm_candidates.argtypes = [ctypes.POINTER(DeviceDesc), ci, ci, ci, ci, ci,
                                           ctypes.c_char_p, ci]
     for fn in (lib.attn_fwd, lib.attn_decode, lib.attn_fwd_ex, lib.attn_decode_ex,
+               lib.attn_decode_noalloc,
                lib.attn_set_stream, lib.attn_query_device,
                lib.attn_measure_device, lib.attn_get_plan, lib.attn_get_plan_for,
                lib.attn__fwd_candidates, lib.attn_gemm, lib.attn_gemm_plan,
@@ -206,6 +209,27 @@ def attn_decode(q, k, v, o=None, n_splits: int = 0, workspace=None, return_lse: 
                               lse.data_ptr() if lse is not None else None, B, Hq, Hkv, Skv, d,
                               int(n_splits), ws_ptr, ws_bytes))
     return (o, lse) if return_lse else o
+
+
+def attn_decode_noalloc(q, k, v, o, n_splits: int = 0, lse=None):
+    """attn_decode with its split partials in the library's static device
+    scratch: allocates nothing, so o (fp32 [B,Hq,d]) and the optional lse
+    (fp32 [B,Hq]) must be given.  Calls that can overlap on one device race
+    on the scratch."""
+    import torch
+    B, Hq, d = q.shape
+    Hkv, Skv = k.shape[1], k.shape[2]
+    _require(q, torch.bfloat16, (B, Hq, d), "q")
+    _require(k, torch.bfloat16, (B, Hkv, Skv, d), "k")
+    _require(v, torch.bfloat16, (B, Hkv, Skv, d), "v")
+    _require(o, torch.float32, (B, Hq, d), "o")
+    if lse is not None:
+        _require(lse, torch.float32, (B, Hq), "lse")
+    _set_stream(q)
+    _check(lib.attn_decode_noalloc(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                   lse.data_ptr() if lse is not None else None, B, Hq, Hkv, Skv,
+                                   d, int(n_splits)))
+    return o
 
 
 def decode_workspace_bytes(B: int, Hq: int, Hkv: int, Skv: int, d: int, n_splits: int = 0) -> int:

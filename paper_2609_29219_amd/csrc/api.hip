@@ -184,6 +184,14 @@ int hip_ws_release(void*, void* stream, void* ptr) {
 
 const WorkspaceMap::Ops kHipWorkspaceOps = {hip_ws_alloc, hip_ws_release, nullptr};
 
+// ---- static decode scratch ---------------------------------------------
+// Device memory for attn_decode_noalloc, the entry point for callers that
+// cannot allocate: a file-scope array that every device the library runs on
+// holds (its own copy, at its own address) until the process ends.  Host
+// code never names it except to look up that address: the name is only a
+// host-side stand-in, and a kernel given it would fault.
+static __device__ __align__(256) float scratch[ATTN_NOALLOC_SCRATCH_BYTES / sizeof(float)];
+
 // ---- per-device state --------------------------------------------------
 // Set up once per device, on the first call made with it current.
 struct DeviceState {
@@ -192,6 +200,8 @@ struct DeviceState {
     bool is_gfx950 = false;
     attn_device_desc desc{};
     WorkspaceMap ws;
+    void* scratch_ptr = nullptr;  // this device's copy of `scratch`
+    hipError_t scratch_err = hipSuccess;
 };
 std::mutex g_mu;  // guards the maps below; never held across a HIP call
 std::map<int, DeviceState> g_devices;  // nodes never move
@@ -228,6 +238,15 @@ int device_state(DeviceState** out) {
     std::call_once(st->once, [&] {
         st->init_err = fill_desc(dev, &st->desc);
         st->is_gfx950 = st->init_err == hipSuccess && strcmp(st->desc.arch, "gfx950") == 0;
+        // the device address of this device's scratch array, looked up once
+        // with the device current (it differs per device)
+        if (st->is_gfx950) {
+            st->scratch_err = hipGetSymbolAddress(&st->scratch_ptr, HIP_SYMBOL(scratch));
+            if (st->scratch_err != hipSuccess) {
+                st->scratch_ptr = nullptr;
+                (void)hipGetLastError();
+            }
+        }
     });
     if (st->init_err != hipSuccess) return fail_hip(st->init_err, "hipGetDeviceProperties");
     if (!st->is_gfx950)
@@ -603,6 +622,34 @@ int attn_decode_ex(const void* q, const void* k, const void* v, float* o, float*
 int attn_decode(const void* q, const void* k, const void* v, float* o, int B, int H, int Skv,
                 int d, int n_splits) {
     return attn_decode_ex(q, k, v, o, nullptr, B, H, H, Skv, d, n_splits, nullptr, 0);
+}
+
+int attn_decode_noalloc(const void* q, const void* k, const void* v, float* o, float* lse, int B,
+                        int Hq, int Hkv, int Skv, int d, int n_splits) {
+    int rc = validate_decode(q, k, v, o, B, Hq, Hkv, Skv, d);
+    if (rc) return rc;
+    if (lse && ((uintptr_t)lse & 3u)) return fail(ATTN_EINVAL, "lse must be 4-byte aligned");
+    DeviceState* st = nullptr;
+    rc = device_state(&st);
+    if (rc) return rc;
+    if (!st->scratch_ptr) return fail_hip(st->scratch_err, "static scratch address");
+    DecodePlan plan;
+    rc = decode_plan(st, B, Hq, Hkv, Skv, d, n_splits, &plan);
+    if (rc) return rc;
+    const size_t ws_bytes = (size_t)B * Hq * plan.n_splits * (d + 2) * sizeof(float);
+    if (ws_bytes > (size_t)ATTN_NOALLOC_SCRATCH_BYTES)
+        return fail(ATTN_ENOMEM,
+                    "this call's decode partials need %zu bytes (%lld rows x %d splits); the "
+                    "static scratch holds %zu",
+                    ws_bytes, (long long)B * Hq, plan.n_splits,
+                    (size_t)ATTN_NOALLOC_SCRATCH_BYTES);
+    // every partial the combine reads is written by the partial kernel first,
+    // so nothing in the scratch needs clearing
+    const float scale = (float)(1.0 / sqrt((double)d));
+    const hipError_t e = launch_decode(plan, q, k, v, o, lse, static_cast<float*>(st->scratch_ptr),
+                                       B, Hq, Hkv, Skv, scale, st->desc.num_xcds, t_stream);
+    if (e != hipSuccess) return fail_hip(e, "decode launch");
+    return ATTN_OK;
 }
 
 // ---------------------------------------------------------------- GEMM --

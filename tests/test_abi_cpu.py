@@ -87,6 +87,24 @@ def test_decode_rejects_on_host(kw, code):
     assert pa.last_error() != ""
 
 
+def dec_noalloc(q=ALIGNED, k=ALIGNED, v=ALIGNED, o=ALIGNED, lse=None, B=1, Hq=2, Hkv=1, Skv=4,
+                d=64, n=0):
+    return pa.lib.attn_decode_noalloc(q, k, v, o, lse, B, Hq, Hkv, Skv, d, n)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(k=None), pa.ATTN_EINVAL),
+    (dict(o=ALIGNED + 4), pa.ATTN_EINVAL),
+    (dict(lse=ALIGNED + 2), pa.ATTN_EINVAL),
+    (dict(Hkv=3), pa.ATTN_EINVAL),
+    (dict(Skv=0), pa.ATTN_EINVAL),
+    (dict(d=96), pa.ATTN_EUNSUPPORTED),
+])
+def test_decode_noalloc_rejects_on_host(kw, code):
+    assert dec_noalloc(**kw) == code
+    assert pa.last_error() != ""
+
+
 def gemm(a=ALIGNED, b=ALIGNED, c=ALIGNED, M=16, N=16, K=16, flags=0):
     return pa.lib.attn_gemm(a, b, c, M, N, K, flags)
 
@@ -113,6 +131,7 @@ def test_valid_call_without_device_is_a_hip_error_not_a_fallback():
     assert fwd(Skv=0x7FFFFFFF // 256, d=128) == pa.ATTN_EHIP
     assert "device" in pa.last_error().lower() or "hip" in pa.last_error().lower()
     assert dec() == pa.ATTN_EHIP
+    assert dec_noalloc() == pa.ATTN_EHIP
     assert gemm() == pa.ATTN_EHIP
 
 
