@@ -3,20 +3,28 @@
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--no-gemm]
     python bench.py --config NAME      # one workload only (own JSON line)
 
-A step is one pass of the whole hot path over one batch of synthetic input:
-prefill attention on B=4 H=16 Sq=Skv=2048 d=128 causal (attn_fwd), then
-Flash-Decode on B=16 H=32 Skv=8192 d=128 (attn_decode: split partials +
-combine).  Inputs are seeded bf16 N(0,1) tensors resident in HBM before the
-timed region.  Each kernel call is bracketed by HIP events on the stream it
-runs on; the step wall time is bracketed by device synchronisation.
+A step is one pass of the whole hot path over one batch of synthetic input,
+on the four full-size workloads:
+  1. prefill B=1 H=32 Sq=Skv=8192 d=128, non-causal, inputs x0.5 (attn_fwd) --
+     the largest prefill workload, the line's headline;
+  2. prefill B=4 H=16 Sq=Skv=2048 d=128, causal (attn_fwd);
+  3. Flash-Decode B=16 H=32 Skv=8192 d=128 (attn_decode: split partials +
+     combine);
+  4. Flash-Decode B=1 H=32 Skv=131072 d=128 (attn_decode).
+Inputs are seeded bf16 tensors resident in HBM before the timed region.  Each
+call is bracketed by HIP events on the stream it runs on; the step wall time
+is bracketed by device synchronisation.  Before the W warmup steps the step
+runs until --prewarm-ms of event-timed GPU work have passed (the clocks leave
+their idle state only after some tens of ms), so the timed steps measure the
+steady state whatever W is.
 
-Printed (one JSON line): value = prefill TFLOP/s (algorithmic flops: 4*d per
-unmasked (query, key) pair) with its MFMA roofline fraction; the decode leg's
-HBM GB/s (algorithmic bytes: K, V, Q read once, O written once) with its HBM
-roofline fraction; the fp64 CPU oracle's rate on a bounded sample of the
-prefill workload, timed on this host's cores; and, timed separately after the
-step, the GEMM workload (C = A B at M = N = K = 8192, bf16 in, fp32 out) with
-its MFMA roofline fraction.
+Printed (one JSON line): value = the headline prefill's TFLOP/s
+(algorithmic flops: 4*d per unmasked (query, key) pair) with its MFMA
+roofline; every leg with its own rate and roofline (MFMA for prefill, HBM
+for decode: K, V, Q read once, O written once); the fp64 CPU oracle's rate on
+a bounded sample of the headline workload, timed on this host's cores; and,
+timed separately after the steps, the GEMM workload (C = A B at
+M = N = K = 8192, bf16 in, fp32 out) with its MFMA roofline.
 """
 from __future__ import annotations
 
@@ -88,13 +96,15 @@ def profiled_mfma_busy(workload: str):
 def _args():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    # the warmup runs the step long enough (~40 ms of GPU time) for the clocks
-    # to leave their idle state; the first few steps after idle run ~20% slower
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=100)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    # the clocks leave their idle state only after some tens of ms of GPU
+    # work (the first steps after idle run ~20% slower), so the step first
+    # runs for this much event-timed GPU time, whatever --warmup says
+    ap.add_argument("--prewarm-ms", type=float, default=200.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gemm", action="store_true", help="skip the GEMM leg")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time for the oracle sample")
     ap.add_argument("--config", default=None, help="bench a single named workload")
     return ap.parse_args()
@@ -168,6 +178,45 @@ def cpu_baseline(w, q, k, v, target_s: float) -> dict:
             "seconds": t}
 
 
+HEADLINE = "prefill_b1_h32_s8192_d128"
+STEP = (HEADLINE, "prefill_b4_h16_s2048_d128_causal", "decode_b16_h32_s8192_d128",
+        "decode_b1_h32_s131072_d128")
+
+
+def _leg(pa, w, dev):
+    """(callable, plan line) for one workload on inputs resident in HBM."""
+    import torch
+    _, _, _, qd, kd, vd = _load_workload(w, dev)
+    if w.kind == "fwd":
+        o = torch.empty((w.B, w.H, w.Sq, w.d), dtype=torch.float32, device=dev)
+        plan = pa.get_plan(pa.KIND_FWD, w.B, w.H, w.Sq, w.Skv, w.d, w.causal)
+        return (lambda: pa.attn_fwd(qd, kd, vd, o=o, scale=w.scale, causal=w.causal)), plan
+    o = torch.empty((w.B, w.H, w.d), dtype=torch.float32, device=dev)
+    plan = pa.get_plan(pa.KIND_DECODE, w.B, w.H, 1, w.Skv, w.d)
+    return (lambda: pa.attn_decode(qd, kd, vd, o=o)), plan
+
+
+def _leg_record(w, ms: float, plan: str) -> dict:
+    """Rate and roofline of one leg from its mean per-call device time."""
+    shape = {"B": w.B, "H": w.H, "Sq": w.Sq, "Skv": w.Skv, "d": w.d, "causal": w.causal}
+    if w.kind == "fwd":
+        tflops = w.flops() / (ms * 1e-3) / 1e12
+        return {"value": tflops, "unit": "TFLOP/s", "ms_per_call": ms, **shape, "plan": plan,
+                "roofline": {"bound": "mfma", "achieved": tflops, "peak": PEAK_BF16_TFLOPS,
+                             "unit": "TFLOP/s", "frac": tflops / PEAK_BF16_TFLOPS,
+                             "traffic": profiled_traffic("prefill", w.name),
+                             "algorithmic_bytes": w.hbm_bytes(), "kernel": "fwd_kernel",
+                             "ms_per_launch": ms, "flops_per_launch": w.flops(),
+                             "mfma_busy_fraction": profiled_mfma_busy(w.name)}}
+    gbs = w.hbm_bytes() / (ms * 1e-3) / 1e9
+    return {"value": gbs, "unit": "GB/s", "ms_per_call": ms, **shape, "plan": plan,
+            "roofline": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                         "frac": gbs / PEAK_HBM_GBS,
+                         "traffic": profiled_traffic("decode", w.name),
+                         "kernel": "decode_partial_kernel + split_combine_kernel",
+                         "bytes_per_call": w.hbm_bytes()}}
+
+
 def main():
     a = _args()
     if a.gpus != 1:
@@ -185,15 +234,7 @@ def main():
         return
     if a.config:
         w = BY_NAME[a.config]
-        q, k, v, qd, kd, vd = _load_workload(w, dev)
-        if w.kind == "fwd":
-            o = torch.empty((w.B, w.H, w.Sq, w.d), dtype=torch.float32, device=dev)
-            fn = lambda: pa.attn_fwd(qd, kd, vd, o=o, scale=w.scale, causal=w.causal)  # noqa: E731
-            plan = pa.get_plan(pa.KIND_FWD, w.B, w.H, w.Sq, w.Skv, w.d, w.causal)
-        else:
-            o = torch.empty((w.B, w.H, w.d), dtype=torch.float32, device=dev)
-            fn = lambda: pa.attn_decode(qd, kd, vd, o=o)  # noqa: E731
-            plan = pa.get_plan(pa.KIND_DECODE, w.B, w.H, 1, w.Skv, w.d)
+        fn, plan = _leg(pa, w, dev)
         mean_ms, med_ms, wall = _time_calls(fn, a.steps, a.warmup)
         rec = {"workload": w.name, "ms_mean": mean_ms, "ms_median": med_ms,
                "ms_wall_per_call": wall, "plan": plan}
@@ -205,75 +246,73 @@ def main():
         print(json.dumps(rec), flush=True)
         return
 
-    wp, wd = BY_NAME["prefill_b4_h16_s2048_d128_causal"], BY_NAME["decode_b16_h32_s8192_d128"]
-    qp, kp, vp, qpd, kpd, vpd = _load_workload(wp, dev)
-    _, _, _, qdd, kdd, vdd = _load_workload(wd, dev)
-    op = torch.empty((wp.B, wp.H, wp.Sq, wp.d), dtype=torch.float32, device=dev)
-    od = torch.empty((wd.B, wd.H, wd.d), dtype=torch.float32, device=dev)
+    ws = [BY_NAME[n] for n in STEP]
+    legs = [_leg(pa, w, dev) for w in ws]
+    fns = [fn for fn, _ in legs]
 
-    def fwd():
-        pa.attn_fwd(qpd, kpd, vpd, o=op, scale=wp.scale, causal=wp.causal)
+    def step():
+        for fn in fns:
+            fn()
 
-    def dec():
-        pa.attn_decode(qdd, kdd, vdd, o=od)
-
-    for _ in range(a.warmup):
-        fwd()
-        dec()
-    torch.cuda.synchronize()
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(a.steps)]
-    t0 = time.perf_counter()
-    for e0, e1, e2 in ev:
+    # pre-warm by GPU time, then the warmup steps
+    pre_ms, pre_steps = 0.0, 0
+    while pre_ms < a.prewarm_ms:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
-        fwd()
+        for _ in range(8):
+            step()
         e1.record()
-        dec()
-        e2.record()
+        torch.cuda.synchronize()
+        pre_ms += e0.elapsed_time(e1)
+        pre_steps += 8
+    for _ in range(a.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(fns) + 1)]
+          for _ in range(a.steps)]
+    t0 = time.perf_counter()
+    for marks in ev:
+        marks[0].record()
+        for i, fn in enumerate(fns):
+            fn()
+            marks[i + 1].record()
     torch.cuda.synchronize()
     ms_per_step = (time.perf_counter() - t0) / a.steps * 1e3
-    fwd_ms = sum(e0.elapsed_time(e1) for e0, e1, _ in ev) / a.steps
-    dec_ms = sum(e1.elapsed_time(e2) for _, e1, e2 in ev) / a.steps
+    leg_ms = [sum(m[i].elapsed_time(m[i + 1]) for m in ev) / a.steps for i in range(len(fns))]
 
-    tflops = wp.flops() / (fwd_ms * 1e-3) / 1e12
-    gbs = wd.hbm_bytes() / (dec_ms * 1e-3) / 1e9
-    fplan = pa.get_plan(pa.KIND_FWD, wp.B, wp.H, wp.Sq, wp.Skv, wp.d, wp.causal)
-    dplan = pa.get_plan(pa.KIND_DECODE, wd.B, wd.H, 1, wd.Skv, wd.d)
+    recs = {w.name: _leg_record(w, ms, plan) for w, ms, (_, plan) in zip(ws, leg_ms, legs)}
+    head = recs[HEADLINE]
+    wh = BY_NAME[HEADLINE]
+    roof = dict(head["roofline"])
+    roof["peak_from_device"] = device_peak(pa)
     rec = {
         "metric": "Attention TFLOP/s + % MFMA peak (prefill); KV HBM GB/s + % peak (decode)",
-        "value": tflops,
+        "value": head["value"],
         "unit": "TFLOP/s",
         "n_gpus": 1,
         "steps": a.steps,
         "warmup": a.warmup,
+        "prewarm_ms": pre_ms,
+        "prewarm_steps": pre_steps,
         "ms_per_step": ms_per_step,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
-        "data": "synthetic (seeded bf16 N(0,1), resident in HBM)",
-        "config": {"workload": f"{wp.name} + {wd.name}",
-                   "prefill": {"B": wp.B, "H": wp.H, "Sq": wp.Sq, "Skv": wp.Skv, "d": wp.d,
-                               "causal": wp.causal, "plan": fplan},
-                   "decode": {"B": wd.B, "H": wd.H, "Skv": wd.Skv, "d": wd.d, "plan": dplan}},
-        "roofline": {"bound": "mfma", "achieved": tflops, "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": tflops / PEAK_BF16_TFLOPS,
-                     "traffic": profiled_traffic("prefill", wp.name),
-                     "algorithmic_bytes": wp.hbm_bytes(),
-                     "kernel": "fwd_kernel", "ms_per_launch": fwd_ms,
-                     "flops_per_launch": wp.flops(),
-                     "mfma_busy_fraction": profiled_mfma_busy(wp.name),
-                     "peak_from_device": device_peak(pa)},
-        "decode": {"value": gbs, "unit": "GB/s", "ms_per_call": dec_ms,
-                   "roofline": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS,
-                                "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS,
-                                "traffic": profiled_traffic("decode", wd.name),
-                                "kernel": "decode_partial_kernel + split_combine_kernel",
-                                "bytes_per_call": wd.hbm_bytes()}},
+        "data": "synthetic (seeded bf16 N(0,1), x0.5 for the long prefill; resident in HBM)",
+        "config": {"workload": HEADLINE, "step": list(STEP),
+                   "B": wh.B, "H": wh.H, "Sq": wh.Sq, "Skv": wh.Skv, "d": wh.d,
+                   "causal": wh.causal, "plan": head["plan"]},
+        "roofline": roof,
+        "legs": recs,
     }
     if not a.no_gemm:
         rec["gemm"] = gemm_leg(pa, dev)
     if not a.no_cpu_baseline:
-        rec["cpu_baseline"] = cpu_baseline(wp, qp, kp, vp, a.cpu_seconds)
+        from attn_inputs import make_inputs
+        q, k, v = make_inputs(wh)
+        rec["cpu_baseline"] = cpu_baseline(wh, q, k, v, a.cpu_seconds)
     print(json.dumps(rec), flush=True)
 
 

@@ -22,7 +22,8 @@ def test_bench_refuses_more_than_one_gpu():
 @pytest.mark.gpu
 def test_bench_line_has_the_contract_fields():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--steps", "3",
-                        "--warmup", "2", "--no-gemm", "--cpu-seconds", "0.5"],
+                        "--warmup", "2", "--prewarm-ms", "20", "--no-gemm", "--cpu-seconds",
+                        "0.5"],
                        capture_output=True, text=True, timeout=600, cwd=ROOT)
     assert r.returncode == 0, r.stderr[-2000:]
     lines = [l for l in r.stdout.splitlines() if l.strip()]
@@ -34,7 +35,8 @@ def test_bench_line_has_the_contract_fields():
         assert key in rec, key
     assert rec["n_gpus"] == 1 and rec["steps"] == 3 and rec["warmup"] == 2
     assert rec["value"] > 0 and rec["unit"] == "TFLOP/s" and rec["higher_is_better"] is True
-    assert "workload" in rec["config"]
+    assert rec["config"]["workload"] == "prefill_b1_h32_s8192_d128"
+    assert rec["prewarm_ms"] >= 20
     roof = rec["roofline"]
     for key in ("bound", "achieved", "peak", "unit", "frac", "traffic"):
         assert key in roof, key
@@ -44,4 +46,10 @@ def test_bench_line_has_the_contract_fields():
     for key in ("value", "unit", "cores", "kind", "sample"):
         assert key in cpu, key
     assert cpu["kind"] == "oracle" and cpu["cores"] >= 1 and cpu["value"] > 0
-    assert rec["decode"]["roofline"]["bound"] == "hbm"
+    legs = rec["legs"]
+    assert set(legs) == {"prefill_b1_h32_s8192_d128", "prefill_b4_h16_s2048_d128_causal",
+                         "decode_b16_h32_s8192_d128", "decode_b1_h32_s131072_d128"}
+    assert legs["prefill_b1_h32_s8192_d128"]["value"] == rec["value"]
+    for name, leg in legs.items():
+        assert leg["roofline"]["bound"] == ("hbm" if name.startswith("decode") else "mfma")
+        assert leg["value"] > 0 and leg["ms_per_call"] > 0
