@@ -129,6 +129,21 @@ __device__ __forceinline__ void static_for(F&& f) {
 
 constexpr int fwd_slots(int pipe) { return pipe == 0 ? 1 : 2; }
 
+// Software-pipeline lag (0, 1 or 2 slots) between the exponentials of a
+// probability pair and its rounding: the largest for which every pair is
+// still rounded in a slot before the first PV MFMA of its 16-key step (the
+// pair's work follows the slot's MFMA in program order); -1 if even lag 0
+// violates that.
+constexpr int fwd_pair_lag(int npair, int exp_slots, int ns, int cb) {
+    for (int lag = 2; lag >= 0; --lag) {
+        bool ok = true;
+        for (int pp = 0; pp < npair; ++pp)
+            if (pp * exp_slots / npair + lag >= ns + (pp / 4) * cb) ok = false;
+        if (ok) return lag;
+    }
+    return -1;
+}
+
 // Waves per SIMD the register allocator should leave room for: two when two
 // workgroups' LDS fits in one CU (or one 8-wave workgroup), else one.
 template <int D, int BN, int NW, int PIPE>
@@ -478,9 +493,11 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     // -inf and the scale is > 0, so they give exactly 0.
     auto rounded_pair = [&](float x0, float x1, bf16x8& dst, int e, float& r0, float& r1)
         __attribute__((always_inline)) {
-        dst[e] = (__bf16)x0;
-        dst[e + 1] = (__bf16)x1;
-        const uint32_t w = __builtin_bit_cast(uint32_t, bf16x2{dst[e], dst[e + 1]});
+        // one packed conversion; both halves are read back from it
+        const bf16x2 pk = {(__bf16)x0, (__bf16)x1};
+        dst[e] = pk[0];
+        dst[e + 1] = pk[1];
+        const uint32_t w = __builtin_bit_cast(uint32_t, pk);
         r0 += __uint_as_float(w << 16);
         r1 += __uint_as_float(w & 0xffff0000u);
     };
@@ -544,9 +561,14 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
         constexpr int MAX0 = EXP_SLOTS + 1;              // first slot carrying the next max
         constexpr int NMAXV = HAS_S ? KB * 16 : 0;      // scores of tile t+1 per lane
         static_assert(!HAS_S || MAX0 < NM, "too few MFMAs to carry the softmax");
-        // pair pp (16-key step pp / 4) is computed in slot pp * EXP_SLOTS / NPAIR,
-        // before the first PV MFMA of its step, NS + (pp / 4) * CB
-        static_assert(!HAS_S || (NPAIR - 1) * EXP_SLOTS / NPAIR < NS + ((NPAIR - 1) / 4) * CB,
+        // The exponentials of pair pp (16-key step pp / 4) are taken in slot
+        // pp * EXP_SLOTS / NPAIR and rounded and summed LAG slots later, so the
+        // rounding does not wait on a just-issued exponential; the rounded
+        // pair must still precede the first PV MFMA of its step, in slot
+        // NS + (pp / 4) * CB.
+        // (not with four waves: their 64-key kernel then spills)
+        constexpr int LAG = HAS_S && NW == 8 ? fwd_pair_lag(NPAIR, EXP_SLOTS, NS, CB) : 0;
+        static_assert(!HAS_S || fwd_pair_lag(NPAIR, EXP_SLOTS, NS, CB) >= 0,
                       "probabilities must precede their PV MFMAs");
         auto fetch = [&](int i) __attribute__((always_inline)) -> bf16x8 {
             if (i < NS) {
@@ -563,15 +585,22 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
             return __builtin_bit_cast(bf16x8, w);
         };
         float mx = -INFINITY, rs0 = 0.f, rs1 = 0.f;
-        auto pair = [&](int pp) __attribute__((always_inline)) {
+        float xe[NPAIR][2];  // exponentials waiting LAG slots for rounding
+        auto exps = [&](int pp) __attribute__((always_inline)) {
             const int kb = pp / 8, h2 = (pp / 4) % 2, e = 2 * (pp % 4);
-            rounded_pair(__builtin_amdgcn_exp2f(fmaf(s_cur[kb][8 * h2 + e], scale_log2, -m_ref)),
-                         __builtin_amdgcn_exp2f(fmaf(s_cur[kb][8 * h2 + e + 1], scale_log2, -m_ref)),
-                         pb[kb][h2], e, rs0, rs1);
+            xe[pp][0] = __builtin_amdgcn_exp2f(fmaf(s_cur[kb][8 * h2 + e], scale_log2, -m_ref));
+            xe[pp][1] = __builtin_amdgcn_exp2f(fmaf(s_cur[kb][8 * h2 + e + 1], scale_log2, -m_ref));
+        };
+        auto round_sum = [&](int pp) __attribute__((always_inline)) {
+            const int kb = pp / 8, h2 = (pp / 4) % 2, e = 2 * (pp % 4);
+            rounded_pair(xe[pp][0], xe[pp][1], pb[kb][h2], e, rs0, rs1);
         };
         if (!HAS_S) {
 #pragma unroll
-            for (int pp = 0; pp < NPAIR; ++pp) pair(pp);
+            for (int pp = 0; pp < NPAIR; ++pp) {
+                exps(pp);
+                round_sum(pp);
+            }
         }
         // causal / ragged-end bound for tile t+1 (MASK_NEXT)
         const int room = (CAUSAL ? min(Skv - 1, qrow + diag) : Skv - 1) - (t + 1) * BN - 16 * hh;
@@ -607,14 +636,22 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
             if constexpr (HAS_S) {
                 static_for<0, NPAIR>([&](auto pc) __attribute__((always_inline)) {
                     constexpr int pp = decltype(pc)::value;
-                    if constexpr (pp * EXP_SLOTS / NPAIR == i) pair(pp);
+                    if constexpr (pp * EXP_SLOTS / NPAIR == i) exps(pp);
+                    if constexpr (pp * EXP_SLOTS / NPAIR + LAG == i) round_sum(pp);
                 });
                 static_for<0, NMAXV>([&](auto vc) __attribute__((always_inline)) {
                     constexpr int v = decltype(vc)::value;
                     if constexpr (MAX0 + v * (NM - MAX0) / NMAXV == i) {
                         if (MASK_NEXT && (v / 16) * 32 + v % 16 > room)
                             s_nxt[v / 16][v % 16] = -INFINITY;
-                        mx = fmaxf(mx, s_nxt[v / 16][v % 16]);
+                        // (no quieting of NaNs: the scores are finite or
+                        // -inf, and two maxima fold into one v_maximum3; the
+                        // four-wave 64-key kernel keeps fmaxf, with which it
+                        // does not spill)
+                        if constexpr (NW == 8)
+                            mx = __builtin_elementwise_maximum(mx, s_nxt[v / 16][v % 16]);
+                        else
+                            mx = fmaxf(mx, s_nxt[v / 16][v % 16]);
                     }
                 });
             }
