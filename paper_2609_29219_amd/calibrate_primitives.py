@@ -1,11 +1,13 @@
 """Characterise the compiled prefill tile kernels once on a gfx950 device.
 
     python paper_2609_29219_amd/calibrate_primitives.py [--gemm] [--write [--out FILE]]
+    python paper_2609_29219_amd/calibrate_primitives.py --device [FILE]
 
 For each head dimension and masking mode, every valid tile variant (block
-width, waves, pipeline knob) is timed on one calibration shape -- B1 H32
-S8192 non-causal, B2 H16 S4096 causal -- and its time is divided by the
-analytic model's time for it (the model without these factors).  The ratio
+width, waves, pipeline knob) is timed on one calibration shape -- B2 H16
+Sq = Skv = 4096, non-causal and causal, which is none of the benchmarked
+workloads -- and its time is divided by the analytic model's time for it
+(the model without these factors).  The ratio
 is the variant's per-tile cost factor: the planner multiplies the modelled
 tile cost by it.  This is the paper's primitive characterisation (its
 latency model takes the cost of each primitive from isolated measurements,
@@ -13,7 +15,11 @@ collected once per architecture), applied to the compiled tile kernels; no
 shape is tuned.  --write regenerates csrc/fwd_primitives.inc.  --gemm does the
 same for the GEMM tile kernels (each B layout and pipe setting, alone on a CU
 -- one tile per CU, K = 8192 -- and sharing CUs at M = N = K = 4096) into
-csrc/gemm_primitives.inc.
+csrc/gemm_primitives.inc.  --device runs the library's isolated
+microbenchmarks instead (attn_measure_device: MFMA, fp32 VALU, v_exp_f32, LDS
+read and HBM stream rates) and prints the device description as JSON (and
+writes it to FILE); the planner's built-in gfx950 performance properties are
+the values it measured on an MI355X.
 """
 from __future__ import annotations
 
@@ -27,7 +33,8 @@ sys.path.insert(0, ROOT)
 
 import paper_2609_29219_amd as pa  # noqa: E402
 
-SHAPES = {False: (1, 32, 8192, 8192), True: (2, 16, 4096, 4096)}  # B, H, Sq, Skv
+# B, H, Sq, Skv of the calibration shapes (disjoint from the benchmarked workloads)
+SHAPES = {False: (2, 16, 4096, 4096), True: (2, 16, 4096, 4096)}
 BNS, WAVES, PIPES = (32, 64, 128), (4, 8), (0, 1, 2, 3)
 INC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc", "fwd_primitives.inc")
 
@@ -137,13 +144,34 @@ def main():
     ap.add_argument("--write", action="store_true", help="regenerate csrc/fwd_primitives.inc")
     ap.add_argument("--out", default=None, help="where --write puts the table")
     ap.add_argument("--gemm", action="store_true", help="the GEMM tile kernels instead")
+    ap.add_argument("--device", nargs="?", const="", default=None, metavar="FILE",
+                    help="measure the device description (microbenchmarks) instead")
+    ap.add_argument("--fields", metavar="FILE",
+                    help="JSON {'fields': {name: value}} (as plan_ablation.py --fit-out "
+                         "writes) overriding description fields of the analytic model")
     a = ap.parse_args()
     import torch
     assert torch.cuda.is_available(), "characterisation needs a HIP device"
+    if a.device is not None:
+        import json
+        text = json.dumps(pa.measure_device(), indent=1)
+        print(text)
+        if a.device:
+            with open(a.device, "w") as f:
+                f.write(text + "\n")
+        return None
     if a.gemm:
         return calibrate_gemm(a.write, a.out or GEMM_INC)
     a.out = a.out or INC
     from attn_inputs import random_bf16
+    desc = None
+    if a.fields:
+        import json
+        desc = pa.DeviceDesc()
+        pa.lib.attn_query_device(ctypes.byref(desc))
+        with open(a.fields) as f:
+            for name, val in json.load(f)["fields"].items():
+                setattr(desc, name, float(val))
     table = {}
     for d in (64, 128):
         for causal in (False, True):
@@ -152,8 +180,8 @@ def main():
             k = random_bf16((B, H, Skv, d), 42).cuda()
             v = random_bf16((B, H, Skv, d), 43).cuda()
             o = torch.empty((B, H, Sq, d), dtype=torch.float32, device="cuda")
-            for c in pa.fwd_candidates(B, H, Sq, Skv, d, causal, device_footprint=True,
-                                       analytic_only=True):
+            for c in pa.fwd_candidates(B, H, Sq, Skv, d, causal, desc=desc,
+                                       device_footprint=True, analytic_only=True):
                 if c["KV_SPLITS"] != 1:
                     continue
                 bn, nw, pipe = c["BLOCK_N"], c["WAVES"], c["PIPE"]

@@ -83,19 +83,26 @@ __global__ __launch_bounds__(256) void mb_lds(uint32_t* out, int iters) {
     out[blockIdx.x * blockDim.x + threadIdx.x] = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
 }
 
+// HBM read stream: each workgroup reads its own contiguous share of the
+// buffer with eight non-temporal 16-byte loads per lane in flight, each wave
+// instruction covering 1 KiB of consecutive bytes -- a long sequential read
+// per workgroup, as a decode workgroup streams its key and value rows.
 __global__ __launch_bounds__(256) void mb_hbm(const u32x4* __restrict__ src, long long n16,
                                               uint32_t* out) {
+    constexpr int U = 8;
+    const long long per = (n16 + gridDim.x - 1) / gridDim.x;  // 16-byte chunks per workgroup
+    const long long b0 = (long long)blockIdx.x * per;
+    const long long b1 = b0 + per < n16 ? b0 + per : n16;
     u32x4 acc = {0u, 0u, 0u, 0u};
-    const long long stride = (long long)gridDim.x * blockDim.x;
-    for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += 4 * stride) {
-        u32x4 v[4];
+    for (long long i = b0 + threadIdx.x; i < b1; i += U * 256) {
+        u32x4 v[U];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const long long j = i + u * stride;
-            v[u] = j < n16 ? __builtin_nontemporal_load(src + j) : u32x4{0u, 0u, 0u, 0u};
+        for (int u = 0; u < U; ++u) {
+            const long long j = i + u * 256;
+            v[u] = j < b1 ? __builtin_nontemporal_load(src + j) : u32x4{0u, 0u, 0u, 0u};
         }
 #pragma unroll
-        for (int u = 0; u < 4; ++u) acc ^= v[u];
+        for (int u = 0; u < U; ++u) acc ^= v[u];
     }
     out[blockIdx.x * blockDim.x + threadIdx.x] = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
 }
@@ -128,7 +135,7 @@ hipError_t measure_device(attn_device_desc* d) {
     const int cus = d->num_cus;
     const double clk = d->clock_ghz * 1e9;
     const int blocks = cus * 2;  // two 4-wave workgroups per CU (compute benchmarks)
-    const int hb = cus * 8;      // workgroups of the HBM stream
+    const int hb = cus * 4;      // workgroups of the HBM stream (128 KiB in flight per CU)
     float* fout = nullptr;       // one output word per thread of the largest grid
     hipError_t e = hipMalloc(&fout, (size_t)hb * 256 * sizeof(float));
     if (e != hipSuccess) return e;

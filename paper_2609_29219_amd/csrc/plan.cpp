@@ -49,20 +49,21 @@ void default_desc(attn_device_desc* d) {
     // microbenchmarks of attn_measure_device() measured them on MI355X, in
     // cycles of the nominal clock (the MFMA-bound clock is lower, so the MFMA
     // rate reads below the 4096 flop/clk of the specification)
-    d->mfma_bf16_flops_per_clk_cu = 3452.0;
-    d->valu_lanes_per_clk_simd = 13.8;
+    d->mfma_bf16_flops_per_clk_cu = 3375.0;
+    d->valu_lanes_per_clk_simd = 13.7;
     d->trans_cycles_per_op = 11.9;           // one wave64 v_exp_f32
-    d->lds_bytes_per_clk_cu = 138.0;
+    d->lds_bytes_per_clk_cu = 135.0;
     d->l2_bytes_per_clk_xcd = 2048.0;
-    d->hbm_bytes_per_s = 5.95e12;            // sustained stream read
+    d->hbm_bytes_per_s = 6.98e12;            // sustained sequential read stream
     d->hbm_latency_us = 2.0;
     d->launch_us = 4.0;
     // prefill resource model, calibrated offline on MI355X (plan_ablation.py
-    // --fit over B1 H32 S8192 d128 and causal B2 H16 S4096 d128)
-    d->issue_cycles_per_score = 87.0;
-    d->valu_mfma_overlap = 0.56;
-    d->tile_sync_cycles = 234.0;
-    d->tile_latency_cycles = 687.0;
+    // --only-calibration --fit: the analytic model alone over every candidate
+    // of B2 H16 S4096 d128, non-causal and causal)
+    d->issue_cycles_per_score = 66.0;
+    d->valu_mfma_overlap = 0.428;
+    d->tile_sync_cycles = 220.8;
+    d->tile_latency_cycles = 703.8;
 }
 
 // HEG composition rules: a pipe node with load, body and store stages and
@@ -198,16 +199,23 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
     const double M = 2.0 * (bn / 32) * (d / 16) * mfma_cyc;
     const double V = scores_per_lane * desc.issue_cycles_per_score;
     const double wpw = waves / (double)simds;  // waves of one workgroup per SIMD
-    const double overlap = wg * wpw >= 2.0 ? desc.valu_mfma_overlap : 0.0;
     const double syncs = pipe == 2 ? 2.0 : 1.0;
-    const double compute = wg * (wpw * (M + (1.0 - overlap) * V) + syncs * desc.tile_sync_cycles);
-    const double lds = wg * (waves * 4.0 * bn * d + 4.0 * bn * d) / desc.lds_bytes_per_clk_cu;
-    const double body = std::max(compute, lds);
     const double latency = desc.tile_latency_cycles;
-    // pipe node (load, body, -): knob b_lm open for pipe >= 1
-    // the compiled kernel's measured cost relative to this analytic body
-    const double tile = heg_pipe(latency / wg, body, 0.0, pipe >= 1 ? 1 : 0, 0) *
-                        fwd_prim_scale(d, bn, waves, pipe, causal);
+    const double prim = fwd_prim_scale(d, bn, waves, pipe, causal);
+    // one K/V tile of each of g workgroups resident on a CU: the pipe node
+    // (load, body, -), knob b_lm open for pipe >= 1, times the compiled
+    // kernel's measured cost relative to this analytic body
+    auto tile_cost = [&](int g, double* compute_out, double* lds_out) {
+        const double overlap = g * wpw >= 2.0 ? desc.valu_mfma_overlap : 0.0;
+        const double compute =
+            g * (wpw * (M + (1.0 - overlap) * V) + syncs * desc.tile_sync_cycles);
+        const double lds = g * (waves * 4.0 * bn * d + 4.0 * bn * d) / desc.lds_bytes_per_clk_cu;
+        if (compute_out) *compute_out = compute;
+        if (lds_out) *lds_out = lds;
+        return heg_pipe(latency / g, std::max(compute, lds), 0.0, pipe >= 1 ? 1 : 0, 0) * prim;
+    };
+    double compute = 0.0, lds = 0.0;
+    const double tile = tile_cost(wg, &compute, &lds);
     const double load_q = latency;
 
     // ---- grid: regular (non-causal) or regularised (causal) --------------
@@ -215,8 +223,16 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
     const int chunk_tiles = (p.kv_chunk + bn - 1) / bn;
     double cycles;
     if (!causal) {
-        const double rounds = ceil((double)p.grid / slots);
-        cycles = rounds * (load_q + heg_for(chunk_tiles, tile));
+        // full rounds of wg workgroups per CU, then a last, partial round in
+        // which each CU holds only ceil(tail / CUs) of them (they share the
+        // CU with fewer others, so each of its tiles costs less)
+        const double full = floor((double)p.grid / slots);
+        const double tail = (double)p.grid - full * slots;
+        cycles = full * (load_q + heg_for(chunk_tiles, tile));
+        if (tail > 0.0) {
+            const int r = (int)std::min<double>(wg, ceil(tail / desc.num_cus));
+            cycles += load_q + heg_for(chunk_tiles, tile_cost(r, nullptr, nullptr));
+        }
     } else {
         // workgroups take q-tile pairs (n-1-u, u), which regularises the
         // triangular work: per workgroup the sum of the pair's tile counts
@@ -258,7 +274,7 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
         bound = "lds";
     } else if (pipe == 0 && wg == 1) {
         bound = "latency";
-    } else if (wpw * M >= wpw * (1.0 - overlap) * V) {
+    } else if (M >= (1.0 - (wg * wpw >= 2.0 ? desc.valu_mfma_overlap : 0.0)) * V) {
         bound = "mfma";
     } else {
         bound = "valu";
