@@ -121,9 +121,27 @@ def _cpu_model() -> str:
     return platform.processor()
 
 
-def _time_calls(fn, steps: int, warmup: int):
+def _prewarm(fn, prewarm_ms: float):
+    """Run fn until prewarm_ms of event-timed GPU work have passed (the clocks
+    leave their idle state); returns (GPU ms, calls)."""
+    import torch
+    done_ms, calls = 0.0, 0
+    while done_ms < prewarm_ms:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(8):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        done_ms += e0.elapsed_time(e1)
+        calls += 8
+    return done_ms, calls
+
+
+def _time_calls(fn, steps: int, warmup: int, prewarm_ms: float = 0.0):
     """Per-call device time (ms) from HIP events on the current stream."""
     import torch
+    _prewarm(fn, prewarm_ms)
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
@@ -230,12 +248,13 @@ def main():
     dev = "cuda:0"
     torch.cuda.set_device(0)
     if a.config == GEMM_WORKLOAD:
-        print(json.dumps(gemm_leg(pa, dev, steps=a.steps, warmup=a.warmup)), flush=True)
+        print(json.dumps(gemm_leg(pa, dev, steps=a.steps, warmup=a.warmup,
+                                  prewarm_ms=a.prewarm_ms)), flush=True)
         return
     if a.config:
         w = BY_NAME[a.config]
         fn, plan = _leg(pa, w, dev)
-        mean_ms, med_ms, wall = _time_calls(fn, a.steps, a.warmup)
+        mean_ms, med_ms, wall = _time_calls(fn, a.steps, a.warmup, a.prewarm_ms)
         rec = {"workload": w.name, "ms_mean": mean_ms, "ms_median": med_ms,
                "ms_wall_per_call": wall, "plan": plan}
         if w.kind == "fwd":
@@ -255,16 +274,7 @@ def main():
             fn()
 
     # pre-warm by GPU time, then the warmup steps
-    pre_ms, pre_steps = 0.0, 0
-    while pre_ms < a.prewarm_ms:
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(8):
-            step()
-        e1.record()
-        torch.cuda.synchronize()
-        pre_ms += e0.elapsed_time(e1)
-        pre_steps += 8
+    pre_ms, pre_steps = _prewarm(step, a.prewarm_ms)
     for _ in range(a.warmup):
         step()
     torch.cuda.synchronize()
@@ -326,7 +336,7 @@ def device_peak(pa) -> dict:
             "simds_per_cu": d["simds_per_cu"], "clock_ghz": d["clock_ghz"]}
 
 
-def gemm_leg(pa, dev, steps=20, warmup=10) -> dict:
+def gemm_leg(pa, dev, steps=20, warmup=10, prewarm_ms=0.0) -> dict:
     """The GEMM workload (C = A B, bf16 in, fp32 out) timed on its own after
     the attention step, outside its timed region."""
     import torch
@@ -335,6 +345,7 @@ def gemm_leg(pa, dev, steps=20, warmup=10) -> dict:
     a = random_bf16((M, K), 31).to(dev)
     b = random_bf16((K, N), 32).to(dev)
     c = torch.empty((M, N), dtype=torch.float32, device=dev)
+    _prewarm(lambda: pa.gemm(a, b, c), prewarm_ms)
     for _ in range(warmup):
         pa.gemm(a, b, c)
     torch.cuda.synchronize()
