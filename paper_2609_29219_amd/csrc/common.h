@@ -176,6 +176,12 @@ bool plan_gemm(const attn_device_desc& desc, int M, int N, int K, int b_nk, Gemm
 int plan_gemm_all(const attn_device_desc& desc, int M, int N, int K, int b_nk, GemmPlan* out,
                   int cap, GemmResFn res = nullptr);
 bool gemm_resources(const GemmPlan& p, KernelRes* out);
+// The 256 x 256 tile on 2 x 2 waves is the hand-scheduled GEMM kernel: it
+// runs two to four LDS slots (pipe 1..3) and needs K to be a whole number of
+// k-tiles.
+inline bool gemm_hand_scheduled(int bm, int bn, int wm, int wn) {
+    return bm == 256 && bn == 256 && wm == 2 && wn == 2;
+}
 int format_gemm_plan(const GemmPlan& p, char* buf, int buflen);
 int format_fwd_plan(const FwdPlan& p, char* buf, int buflen);
 int format_decode_plan(const DecodePlan& p, char* buf, int buflen);

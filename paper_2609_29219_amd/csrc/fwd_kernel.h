@@ -118,15 +118,6 @@ __device__ __forceinline__ s16x4 lds_read_tr(const uint16_t* p) {
         (__attribute__((address_space(3))) s16x4*)(p));
 }
 
-// Compile-time loop: f(std::integral_constant<int, I>{}) for I in [B, E).
-template <int B, int E, typename F>
-__device__ __forceinline__ void static_for(F&& f) {
-    if constexpr (B < E) {
-        f(std::integral_constant<int, B>{});
-        static_for<B + 1, E>(f);
-    }
-}
-
 constexpr int fwd_slots(int pipe) { return pipe == 0 ? 1 : 2; }
 
 // Software-pipeline lag (0, 1 or 2 slots) between the exponentials of a

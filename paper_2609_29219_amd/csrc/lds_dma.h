@@ -11,10 +11,15 @@
 // the waits itself: before the barrier that publishes a tile, every wave
 // waits (vmcnt) until its own loads of that tile have landed, and the
 // barrier then makes all waves' loads of it visible.
+//
+// Also the compile-time loop with which the kernels unroll their
+// hand-scheduled MFMA slots.
 #pragma once
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <type_traits>
 
 namespace attn {
 
@@ -72,6 +77,15 @@ template <int N>
 __device__ __forceinline__ void publish_barrier() {
     static_assert(N >= 0 && N < 64, "vmcnt holds 6 bits");
     asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" : : "n"(N) : "memory");
+}
+
+// Compile-time loop: f(std::integral_constant<int, I>{}) for I in [B, E).
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        static_for<B + 1, E>(f);
+    }
 }
 
 }  // namespace attn

@@ -130,7 +130,9 @@ void use_fwd_primitive_costs(bool on) { t_prim_scales = on; }
 // or several workgroups share a CU (a lone workgroup's waves cannot hide
 // each other's stalls, so its tiles cost more than the shared-CU model says).
 static double gemm_prim_scale(int tile, int b_nk, int pipe, bool shared_cu) {
-    if (!t_prim_scales || tile < 0 || tile >= 9 || pipe < 0 || pipe > 2) return 1.0;
+    constexpr int n_tiles = (int)(sizeof kGemmPrimScale / sizeof kGemmPrimScale[0]);
+    constexpr int n_pipes = (int)(sizeof kGemmPrimScale[0][0] / sizeof kGemmPrimScale[0][0][0]);
+    if (!t_prim_scales || tile < 0 || tile >= n_tiles || pipe < 0 || pipe >= n_pipes) return 1.0;
     const double f = kGemmPrimScale[tile][b_nk ? 1 : 0][pipe][shared_cu ? 1 : 0];
     return f > 0.0 ? f : 1.0;
 }
@@ -325,17 +327,22 @@ int plan_fwd_all(const attn_device_desc& desc, int B, int H, int Sq, int Skv, in
 }
 
 // ------------------------------------------------------------------ GEMM --
-// Compiled GEMM tiles (BM, BN, BK, wave grid WM x WN); each exists for both B
-// layouts and for every pipe setting (1, 2 or 3 LDS slots) whose LDS fits.
+// Compiled GEMM tiles (BM, BN, BK, wave grid WM x WN, pipe range); each
+// exists for both B layouts and for every pipe setting in its range (pipe + 1
+// LDS slots) whose LDS fits.  The 256 x 256 tiles on 2 x 2 waves are the
+// hand-scheduled kernel, which needs a second slot.
 struct GemmTile {
-    int bm, bn, bk, wm, wn;
+    int bm, bn, bk, wm, wn, pipe_min, pipe_max;
 };
 static constexpr int kGemmGroupM = 8;  // tile rows per group of the workgroup order
+static constexpr int kGemmPipeMax = 3;
 static constexpr GemmTile kGemmTiles[] = {
-    {64, 64, 64, 2, 2},    {128, 128, 32, 2, 2}, {128, 128, 64, 2, 2},
-    {256, 128, 32, 2, 2},  {256, 128, 64, 2, 2}, {128, 256, 32, 2, 2},
-    {128, 256, 64, 2, 2},  {256, 256, 32, 2, 4}, {256, 256, 64, 2, 4},
+    {64, 64, 64, 2, 2, 0, 2},    {128, 128, 32, 2, 2, 0, 2}, {128, 128, 64, 2, 2, 0, 2},
+    {256, 128, 32, 2, 2, 0, 2},  {256, 128, 64, 2, 2, 0, 2}, {128, 256, 32, 2, 2, 0, 2},
+    {128, 256, 64, 2, 2, 0, 2},  {256, 256, 32, 2, 4, 0, 2}, {256, 256, 64, 2, 4, 0, 2},
+    {256, 256, 32, 2, 2, 1, 3},  {256, 256, 64, 2, 2, 1, 3},
 };
+static constexpr int kGemmNumTiles = (int)(sizeof kGemmTiles / sizeof kGemmTiles[0]);
 
 int gemm_lds_bytes(int bm, int bn, int bk, int b_nk, int pipe) {
     const int a = bm * (bk + 8);
@@ -369,11 +376,14 @@ int gemm_lds_bytes(int bm, int bn, int bk, int b_nk, int pipe) {
 bool plan_gemm_fixed(const attn_device_desc& desc, int M, int N, int K, int b_nk, int bm, int bn,
                      int bk, int wm, int wn, int pipe, GemmPlan* out, GemmResFn res) {
     int tile_index = -1;
-    for (int i = 0; i < (int)(sizeof kGemmTiles / sizeof kGemmTiles[0]); ++i) {
+    for (int i = 0; i < kGemmNumTiles; ++i) {
         const GemmTile& t = kGemmTiles[i];
         if (t.bm == bm && t.bn == bn && t.bk == bk && t.wm == wm && t.wn == wn) tile_index = i;
     }
-    if (tile_index < 0 || pipe < 0 || pipe > 2) return false;
+    if (tile_index < 0 || pipe < kGemmTiles[tile_index].pipe_min ||
+        pipe > kGemmTiles[tile_index].pipe_max)
+        return false;
+    if (gemm_hand_scheduled(bm, bn, wm, wn) && K % bk != 0) return false;
     GemmPlan p;
     p.block_m = bm;
     p.block_n = bn;
@@ -412,11 +422,7 @@ bool plan_gemm_fixed(const attn_device_desc& desc, int M, int N, int K, int b_nk
     const double compute = 2.0 * bm * bn * bk / desc.mfma_bf16_flops_per_clk_cu;
     const double lds_bytes = waves * (double)(mb + nb) * 64.0 * bk + (double)(bm + bn) * bk * 2.0;
     const double lds = lds_bytes / desc.lds_bytes_per_clk_cu;
-    // the compiled kernel's measured cost of a k-tile relative to this
-    // analytic body, alone on a CU or sharing it; load latency and bandwidth
-    // terms stay analytic
-    const double body1 =
-        std::max(compute, lds) * gemm_prim_scale(tile_index, b_nk, pipe, gr >= 2.0);
+    const double body1 = std::max(compute, lds);
     const double body_g = gr * body1 + desc.tile_sync_cycles;
     // HBM share of a k-tile's bytes: the resident tiles of one XCD need each
     // of their distinct A and B panels once
@@ -436,6 +442,12 @@ bool plan_gemm_fixed(const attn_device_desc& desc, int M, int N, int K, int b_nk
     double round = pipe == 0 ? std::max(heg_pipe(load, body1, 0.0, 0, 0), body_g)
                              : heg_pipe(load / pipe, body_g, 0.0, 1, 0);
     round = std::max(round, t_bw);
+    const double round_analytic = round;
+    // the compiled kernel's measured cost of a k-tile round relative to this
+    // analytic one, alone on a CU or sharing it: the factor is measured as a
+    // ratio of whole GEMMs of many k-tiles, so it scales the whole round
+    // (body, exposed latency and bandwidth alike), not the body alone
+    round *= gemm_prim_scale(tile_index, b_nk, pipe, gr >= 2.0);
 
     const int n_k = (K + bk - 1) / bk;
     const double store = gr * (double)bm * bn * 4.0 / cu_bw;
@@ -449,7 +461,7 @@ bool plan_gemm_fixed(const attn_device_desc& desc, int M, int N, int K, int b_nk
     const double l2_us =
         l2_bytes / (desc.l2_bytes_per_clk_xcd * desc.num_xcds * desc.clock_ghz * 1e9) * 1e6;
     const char* bound = lds > compute ? "lds" : "mfma";
-    if (round > body_g) bound = t_bw >= round ? "hbm" : "latency";
+    if (round_analytic > body_g) bound = t_bw >= round_analytic ? "hbm" : "latency";
     if (hbm_us > us) {
         us = hbm_us;
         bound = "hbm";
@@ -468,7 +480,7 @@ int plan_gemm_all(const attn_device_desc& desc, int M, int N, int K, int b_nk, G
                   int cap, GemmResFn res) {
     int n = 0;
     for (const GemmTile& t : kGemmTiles)
-        for (int pipe : {0, 1, 2}) {
+        for (int pipe = t.pipe_min; pipe <= t.pipe_max; ++pipe) {
             GemmPlan p;
             if (!plan_gemm_fixed(desc, M, N, K, b_nk, t.bm, t.bn, t.bk, t.wm, t.wn, pipe, &p, res))
                 continue;
@@ -483,7 +495,7 @@ bool plan_gemm(const attn_device_desc& desc, int M, int N, int K, int b_nk, Gemm
     bool found = false;
     GemmPlan best;
     for (const GemmTile& t : kGemmTiles)
-        for (int pipe : {0, 1, 2}) {
+        for (int pipe = t.pipe_min; pipe <= t.pipe_max; ++pipe) {
             GemmPlan p;
             if (!plan_gemm_fixed(desc, M, N, K, b_nk, t.bm, t.bn, t.bk, t.wm, t.wn, pipe, &p, res))
                 continue;

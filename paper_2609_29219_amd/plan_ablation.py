@@ -307,7 +307,7 @@ def decode_ablation(data: dict, load: bool) -> list:
 GEMM_SHAPES = [(256, 256, 256), (1024, 1024, 1024), (2048, 2048, 2048), (4096, 4096, 4096),
                (8192, 8192, 8192), (16384, 16384, 16384), (16384, 256, 2048), (256, 256, 2048),
                (16384, 256, 16384), (2048, 2048, 16384)]
-GEMM_DOMAINS = ((64, 128, 256), (64, 128, 256), (32, 64), (0, 1, 2))  # BM, BN, BK, pipe
+GEMM_DOMAINS = ((64, 128, 256), (64, 128, 256), (32, 64), (0, 1, 2, 3))  # BM, BN, BK, pipe
 
 
 def gemm_key(c: dict) -> tuple:
@@ -397,22 +397,22 @@ def main_gemm(a):
             raw = json.load(f)
         data = {tuple(map(int, s.split(","))): {tuple(map(int, k.split(","))): t
                                                for k, t in m.items()} for s, m in raw.items()}
-    summaries = []
-    for shape in GEMM_SHAPES:
-        cands = pa.gemm_candidates(*shape)
-        if not a.load:
+    cands = {shape: pa.gemm_candidates(*shape) for shape in GEMM_SHAPES}
+    if not a.load:
+        for shape in GEMM_SHAPES:
             meas = {}
-            for c in cands:
+            for c in cands[shape]:
                 meas[gemm_key(c)] = time_gemm(shape, gemm_key(c))
                 print(f"{shape} {gemm_key(c)} modelled {c['modeled_us']:.1f} us measured "
                       f"{meas[gemm_key(c)]:.1f} us", flush=True)
             data[shape] = meas
-        if shape in data:
-            summaries.append(gemm_summary(shape, cands, data[shape]))
+    # saved before summarising, so a summary error loses no measurement
     if a.save:
         with open(a.save, "w") as f:
             json.dump({",".join(map(str, s)): {",".join(map(str, k)): t for k, t in m.items()}
                        for s, m in data.items()}, f, indent=1)
+    summaries = [gemm_summary(shape, cands[shape], data[shape]) for shape in GEMM_SHAPES
+                 if shape in data]
     text = gemm_markdown(summaries)
     print(text)
     if a.markdown:

@@ -111,14 +111,16 @@ bool check_gemm(const attn_device_desc& desc, const GemmPlan& p, int M, int N, i
     CHECK(p.block_m % (32 * p.waves_m) == 0 && p.block_n % (32 * p.waves_n) == 0,
           "tile %dx%d over %dx%d waves", p.block_m, p.block_n, p.waves_m, p.waves_n);
     CHECK(p.block_k == 32 || p.block_k == 64, "BK %d", p.block_k);
-    CHECK(p.pipe >= 0 && p.pipe <= 2, "pipe %d", p.pipe);
+    // the 256 x 256 tile on 2 x 2 waves (hand-scheduled) runs pipes 1..3, the others 0..2
+    const bool scheduled = p.block_m == 256 && p.block_n == 256 && p.waves_m == 2 && p.waves_n == 2;
+    CHECK(scheduled ? p.pipe >= 1 && p.pipe <= 3 : p.pipe >= 0 && p.pipe <= 2, "pipe %d", p.pipe);
     CHECK(p.lds_bytes > 0 && p.lds_bytes <= desc.lds_bytes_per_cu, "lds %d", p.lds_bytes);
     CHECK(p.tiles_m == (M + p.block_m - 1) / p.block_m &&
               p.tiles_n == (N + p.block_n - 1) / p.block_n,
           "tiles %dx%d", p.tiles_m, p.tiles_n);
     CHECK(p.grid == (long long)p.tiles_m * p.tiles_n, "grid %lld", p.grid);
     CHECK(std::isfinite(p.modeled_us) && p.modeled_us > 0.0, "modeled %g", p.modeled_us);
-    (void)K;
+    CHECK(!scheduled || K % p.block_k == 0, "hand-scheduled tile with K %d not whole k-tiles", K);
     return true;
 }
 
