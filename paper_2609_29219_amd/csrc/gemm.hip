@@ -119,8 +119,10 @@ __device__ __forceinline__ GemmOrigin gemm_origin(const GemmArgs& args, int BM, 
 // source chunk for the wave's j-th piece relative to the k-tile's first
 // element; the tile's own offset is a scalar.  Chunks past K (on the ragged
 // last k-tile only, flagged per piece in this lane's `past_k` bits) read
-// from an offset past the buffer and land as zeros.
-template <int BM, int BN, int BK, int NW, bool B_NK>
+// from an offset past the buffer and land as zeros.  SHIFT_B (B stored
+// [K][N]): the rows of odd 8-row blocks of k hold their data 16 columns to
+// the right inside the row padding (see the hand-scheduled kernel's reads).
+template <int BM, int BN, int BK, int NW, bool B_NK, bool SHIFT_B = false>
 struct GemmLoader {
     using L = GemmLds<BM, BN, BK, B_NK>;
     static constexpr int NP = L::A_PIECES + L::B_PIECES;
@@ -172,9 +174,12 @@ struct GemmLoader {
                 o = (row * K + c * 8) * 2;
                 kc = c * 8;
             } else {
-                // columns past N (outputs never stored) re-read the last chunk of the row
-                const int c = min(min(pos % L::B_CPR, L::B_REAL - 1), (N - n0) / 8 - 1);
+                // columns past N (outputs never stored) re-read the last chunk of the
+                // row, and so do the padding chunks
                 const int r = pos / L::B_CPR;
+                const int shift = SHIFT_B && ((r >> 3) & 1) ? 2 : 0;
+                const int c = min(max(pos % L::B_CPR - shift, 0),
+                                  min(L::B_REAL - 1, (N - n0) / 8 - 1));
                 o = (r * N + c * 8) * 2;
                 kc = r;
             }
@@ -433,7 +438,11 @@ void gemm_kernel(const GemmArgs args) {
 // reads, or one 16-byte read when B is stored [N][K]), its B operand row m =
 // l % 16 of a 16-row block of A at the same k (one 16-byte read); the
 // accumulator then holds, in register r of lane l, C at row l % 16 and
-// column 4 (l / 16) + r of the block.
+// column 4 (l / 16) + r of the block.  In a transposed read, lanes 16..31
+// address rows 8 below lanes 0..15; B rows are 144 banks apart (576 bytes),
+// so those rows would fall on the same banks, and no linear padding keeps
+// all eight rows of a read apart: the odd 8-row blocks of k are therefore
+// stored 16 columns (8 banks) to the right inside the row padding.
 //
 // The k-loop is scheduled by hand at MFMA granularity: a step is 64 MFMAs
 // (block (nb, mb) in slot 8 nb + mb), each slot its own scheduling region,
@@ -565,9 +574,10 @@ __global__ __launch_bounds__(256, 1) void gemm_sched_kernel(const GemmArgs args)
     constexpr int NSLOT = PIPE + 1;
     constexpr int KS = BK / 32;        // 32-k steps per k-tile
     constexpr int NM = MB16 * NB16;    // MFMA slots per step
-    using Ld = GemmLoader<BM, BN, BK, NW, B_NK>;
+    using Ld = GemmLoader<BM, BN, BK, NW, B_NK, !B_NK>;
     using L = GemmLds<BM, BN, BK, B_NK>;
     constexpr int SLOT = Ld::SLOT;
+    static_assert(B_NK || BN + 16 <= L::B_STRIDE, "the shifted rows fit the padding");
     constexpr int PHASES = NSLOT >= 3 ? KS : 1;  // steps a tile's loads are spread over
     static_assert(NSLOT >= 2 && NSLOT <= 4, "two to four LDS slots");
     static_assert(KS == 1 || KS == 2, "k-tiles of 32 or 64");
@@ -585,7 +595,7 @@ __global__ __launch_bounds__(256, 1) void gemm_sched_kernel(const GemmArgs args)
     const int a_off = (wm0 + (lane & 15)) * L::A_STRIDE + 8 * (lane >> 4);
     const int b_off = B_NK ? L::A_TILE + (wn0 + (lane & 15)) * L::B_STRIDE + 8 * (lane >> 4)
                            : L::A_TILE + (8 * (lane >> 4) + ((lane & 15) >> 2)) * L::B_STRIDE +
-                                 wn0 + 4 * (lane & 3);
+                                 wn0 + 4 * (lane & 3) + 16 * ((lane >> 4) & 1);
     // waves below this index load NJ pieces per tile, the others NJ_MIN
     const bool more = wave < Ld::NP - Ld::NJ_MIN * NW;
 
