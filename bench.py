@@ -318,7 +318,8 @@ def main():
         "legs": recs,
     }
     if not a.no_gemm:
-        rec["gemm"] = gemm_leg(pa, dev)
+        # the same time-based pre-warm as the attention step
+        rec["gemm"] = gemm_leg(pa, dev, prewarm_ms=a.prewarm_ms)
     if not a.no_cpu_baseline:
         from attn_inputs import make_inputs
         q, k, v = make_inputs(wh)
