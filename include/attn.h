@@ -260,17 +260,23 @@ int attn_get_plan_for(const attn_device_desc* desc, int kind, int B, int H, int 
  *   c: [M][N] row-major, fp32, or bf16 with ATTN_OUT_BF16 (caller-allocated,
  *      fully overwritten).
  * Work: bf16 MFMA products with fp32 accumulation (blocked summation order),
- * rounded once to the output type.  Supported: M >= 1, N and K multiples of
- * 8 (16-byte rows), A and B each at most 2 GiB.  Asynchronous on the
- * thread's stream; allocates nothing.
+ * rounded once to the output type.  When the plan splits K (K_SPLITS > 1 in
+ * attn_gemm_plan: few output tiles, long K), each split's fp32 partial goes
+ * to the library's per-stream workspace (stream-ordered allocation, grown
+ * as for decode) and a second kernel sums the partials in split order, so
+ * the result is the same for every call with that plan.  Supported: M >= 1,
+ * N and K multiples of 8 (16-byte rows), A and B each at most 2 GiB.
+ * Asynchronous on the thread's stream.
  * Errors: EINVAL for null or misaligned pointers, dims <= 0 or unknown
  * flags; EUNSUPPORTED for N or K not a multiple of 8, operands over 2 GiB,
- * or a device that is not gfx950; EHIP for launch errors.
+ * or a device that is not gfx950; ENOMEM if a split plan's workspace cannot
+ * be allocated; EHIP for launch errors.
  */
 int attn_gemm(const void* a, const void* b, void* c, int M, int N, int K, int flags);
 
 /* GEMM plan query (host only): the named tile symbols BLOCK_M, BLOCK_N,
- * BLOCK_K, WAVES_M, WAVES_N, PIPE, the grid, the modelled time in us and the
+ * BLOCK_K, WAVES_M, WAVES_N, PIPE, K_SPLITS (with the k values per split),
+ * the grid, the modelled time in us and the
  * binding resource, as one NUL-terminated line in buf (truncated to buflen).
  * desc NULL: this device's description and its compiled kernels' real
  * register/occupancy footprint.  Returns the full line length or a

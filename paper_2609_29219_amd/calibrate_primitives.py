@@ -119,10 +119,12 @@ def calibrate_gemm(write: bool, out: str) -> None:
                             c["WAVES_N"]) == tile]
                     if one_per_cu and all(one_per_cu):
                         M *= 2
+                # (unsplit K: the factor is the per-k-tile cost of the tile kernel)
                 cands = [c for c in pa.gemm_candidates(M, N, K, b_nk, device_footprint=True,
                                                        analytic_only=True)
                          if (c["BLOCK_M"], c["BLOCK_N"], c["BLOCK_K"], c["WAVES_M"],
-                             c["WAVES_N"]) == tile and (not shared or c["wg_per_cu"] >= 2)]
+                             c["WAVES_N"]) == tile and c.get("K_SPLITS", 1) == 1
+                         and (not shared or c["wg_per_cu"] >= 2)]
                 if not cands:
                     continue  # (sharing: a tile that cannot share a CU has the alone setting only)
                 a = random_bf16((M, K), 51).cuda()

@@ -276,12 +276,15 @@ int stream_workspace(DeviceState* st, size_t bytes, std::unique_lock<std::mutex>
 }
 
 // Optional fixed GEMM tile for the block-size ablation only:
-// ATTN_FORCE_GEMM="bm=256,bn=256,bk=64,wm=2,wn=4,pipe=1".  Never used to
-// select tiles.
-bool forced_gemm(int* bm, int* bn, int* bk, int* wm, int* wn, int* pipe) {
+// ATTN_FORCE_GEMM="bm=256,bn=256,bk=64,wm=2,wn=4,pipe=1[,splits=4]".  Never
+// used to select tiles.
+bool forced_gemm(int* bm, int* bn, int* bk, int* wm, int* wn, int* pipe, int* splits) {
     const char* s = getenv("ATTN_FORCE_GEMM");
     if (!s || !*s) return false;
-    return sscanf(s, "bm=%d,bn=%d,bk=%d,wm=%d,wn=%d,pipe=%d", bm, bn, bk, wm, wn, pipe) == 6;
+    *splits = 1;
+    const int n =
+        sscanf(s, "bm=%d,bn=%d,bk=%d,wm=%d,wn=%d,pipe=%d,splits=%d", bm, bn, bk, wm, wn, pipe, splits);
+    return n == 6 || n == 7;
 }
 
 // Forced tiles (ablation only) may run a variant that spills: slow, not wrong.
@@ -730,10 +733,10 @@ int attn_gemm(const void* a, const void* b, void* c, int M, int N, int K, int fl
     if (rc) return rc;
     const int b_nk = (flags & ATTN_GEMM_B_NK) ? 1 : 0;
     GemmPlan plan;
-    int bm, bn, bk, wm, wn, pipe;
-    if (forced_gemm(&bm, &bn, &bk, &wm, &wn, &pipe)) {
+    int bm, bn, bk, wm, wn, pipe, splits;
+    if (forced_gemm(&bm, &bn, &bk, &wm, &wn, &pipe, &splits)) {
         if (!plan_gemm_fixed(st->desc, M, N, K, b_nk, bm, bn, bk, wm, wn, pipe, &plan,
-                             gemm_resources_forced))
+                             gemm_resources_forced, splits))
             return fail(ATTN_EINVAL, "ATTN_FORCE_GEMM names an infeasible or unknown tile");
     } else {
         const auto key = std::make_tuple(M, N, K, b_nk, st->desc.num_cus);
@@ -750,8 +753,14 @@ int attn_gemm(const void* a, const void* b, void* c, int M, int N, int K, int fl
             g_gemm_cache[key] = plan;
         }
     }
+    void* ws = nullptr;
+    std::unique_lock<std::mutex> ws_lock;  // held until the kernels are enqueued
+    if (plan.k_splits > 1) {
+        rc = stream_workspace(st, (size_t)gemm_workspace_bytes(plan, M, N), &ws_lock, &ws);
+        if (rc) return rc;
+    }
     const hipError_t e = launch_gemm(plan, a, b, c, M, N, K, (flags & ATTN_OUT_BF16) ? 1 : 0,
-                                     st->desc.num_xcds, t_stream);
+                                     st->desc.num_xcds, static_cast<float*>(ws), t_stream);
     if (e != hipSuccess) return fail_hip(e, "GEMM launch");
     return ATTN_OK;
 }

@@ -55,10 +55,20 @@ struct GemmPlan {
     int vgprs = 0;
     int wg_per_cu = 0;
     int tiles_m = 0, tiles_n = 0;
+    // K split (hand-scheduled tiles only): k_splits workgroups per tile each
+    // take k_chunk values of k (whole k-tiles; the last split may hold fewer)
+    // and write an fp32 partial tile to the workspace; a reduction then sums
+    // the partials in split order into C
+    int k_splits = 1, k_chunk = 0;
     long long grid = 0;
     double modeled_us = 0.0;
     const char* bound = "";
 };
+
+// Workspace bytes of a GEMM plan (the partials of a K split; 0 unsplit).
+inline long long gemm_workspace_bytes(const GemmPlan& p, int M, int N) {
+    return p.k_splits > 1 ? (long long)p.k_splits * M * N * 4 : 0;
+}
 
 // Arguments of one GEMM launch.
 struct GemmArgs {
@@ -70,6 +80,11 @@ struct GemmArgs {
     int n_wg;
     int num_xcds;
     int out_bf16;
+    // K split: workgroup w takes split w / (tiles_m tiles_n) of the grid's
+    // split-major order; partial s of C goes to ws + s M N (fp32, [M][N])
+    int k_splits;
+    int k_chunk;
+    float* ws;
 };
 
 // Candidate domains: every point is an instantiated kernel.
@@ -149,6 +164,9 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
 // non-empty with a chunk that is a multiple of the tile width, and the split
 // grid must stay within kFwdSplitRounds rounds of the CUs).
 constexpr int kFwdKvSplits[] = {1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48, 64, 96, 128, 192, 256};
+// GEMM K splits (hand-scheduled tiles) and the workspace they may use
+constexpr int kGemmKSplits[] = {1, 2, 3, 4, 6, 8};
+constexpr long long kGemmMaxWorkspaceBytes = 1LL << 30;
 constexpr int kFwdSplitRounds = 4;
 // Bytes of the split-KV workspace: rows * splits * (d + 2) floats (the
 // partial outputs, then the maxima, then the sums).
@@ -170,7 +188,8 @@ bool plan_decode(const attn_device_desc& desc, int B, int Hq, int Hkv, int Skv, 
 // footprint.
 typedef bool (*GemmResFn)(const GemmPlan& p, KernelRes* out);
 bool plan_gemm_fixed(const attn_device_desc& desc, int M, int N, int K, int b_nk, int bm, int bn,
-                     int bk, int wm, int wn, int pipe, GemmPlan* out, GemmResFn res = nullptr);
+                     int bk, int wm, int wn, int pipe, GemmPlan* out, GemmResFn res = nullptr,
+                     int k_splits = 1);
 bool plan_gemm(const attn_device_desc& desc, int M, int N, int K, int b_nk, GemmPlan* out,
                GemmResFn res = nullptr);
 int plan_gemm_all(const attn_device_desc& desc, int M, int N, int K, int b_nk, GemmPlan* out,
@@ -202,8 +221,10 @@ hipError_t launch_split_combine(int d, const float* ws_m, const float* ws_l, con
 hipError_t launch_decode(const DecodePlan& p, const void* q, const void* k, const void* v,
                          float* o, float* lse, float* workspace, int B, int Hq, int Hkv, int Skv,
                          float scale, int num_xcds, hipStream_t stream);
+// With p.k_splits > 1, workspace holds gemm_workspace_bytes(p, M, N) bytes
+// and the reduction of the partials follows on the same stream.
 hipError_t launch_gemm(const GemmPlan& p, const void* a, const void* b, void* c, int M, int N,
-                       int K, int out_bf16, int num_xcds, hipStream_t stream);
+                       int K, int out_bf16, int num_xcds, float* workspace, hipStream_t stream);
 // Query heads of one key/value group that a decode workgroup serves together.
 int decode_heads_per_wg(int group);
 

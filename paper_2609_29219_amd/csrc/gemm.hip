@@ -90,27 +90,31 @@ struct GemmLds {
     static_assert(A_TILE % 512 == 0 && B_TILE % 512 == 0, "whole wave loads per tile");
 };
 
-// Tile of C computed by this workgroup: the hardware deals workgroup ids
-// round-robin to the XCDs; each XCD takes a contiguous range of logical
-// tiles, which run down groups of kGroupM tile rows before moving right.
+// Tile of C (and K split) computed by this workgroup: the hardware deals
+// workgroup ids round-robin to the XCDs; each XCD takes a contiguous range of
+// logical indices, split-major (so an XCD's tiles share one K range of the
+// panels), whose tiles run down groups of kGroupM tile rows before moving
+// right.
 struct GemmOrigin {
-    int m0, n0;
+    int m0, n0, split;
 };
 __device__ __forceinline__ GemmOrigin gemm_origin(const GemmArgs& args, int BM, int BN) {
     const int n_wg = args.n_wg, num_xcds = args.num_xcds;
     const int wg = blockIdx.x;
     const int per = n_wg / num_xcds, rem = n_wg % num_xcds;
     const int xcd = wg % num_xcds, slot_id = wg / num_xcds;
-    const int logical =
+    const int index =
         (xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per) + slot_id;
     const int tiles_m = args.tiles_m, tiles_n = args.tiles_n;
+    const int split = index / (tiles_m * tiles_n);
+    const int logical = index - split * (tiles_m * tiles_n);
     const int group = logical / (kGroupM * tiles_n);
     const int first_m = group * kGroupM;
     const int gsize = min(tiles_m - first_m, kGroupM);
     const int in_group = logical - group * kGroupM * tiles_n;
     const int tm = first_m + in_group % gsize;
     const int tn = in_group / gsize;
-    return {tm * BM, tn * BN};
+    return {tm * BM, tn * BN, split};
 }
 
 // Direct-to-LDS loads of the k-tiles.  A k-tile's A and B regions are cut
@@ -140,8 +144,10 @@ struct GemmLoader {
     int off[NJ];
     uint32_t past_k;
 
+    // k0: the first k this workgroup multiplies (its K split's), a whole
+    // number of k-tiles
     __device__ __forceinline__ GemmLoader(const GemmArgs& args, const uint16_t* lds, int wave_,
-                                          int lane, int m0, int n0)
+                                          int lane, int m0, int n0, int k0 = 0)
         : wave(wave_) {
         // with the wave index bounded, whether piece j is an A or a B piece,
         // or missing, folds at compile time wherever the counts allow
@@ -151,9 +157,10 @@ struct GemmLoader {
         b_rsrc = make_dma_rsrc(args.b, (uint32_t)((long long)N * K * 2));
         lds0 = lds_address(lds);
         // 32-bit offsets: A and B are under 2 GiB each (checked on the host)
-        a_tile0 = __builtin_amdgcn_readfirstlane((uint32_t)m0 * (uint32_t)K * 2u);
-        b_tile0 = __builtin_amdgcn_readfirstlane(B_NK ? (uint32_t)n0 * (uint32_t)K * 2u
-                                                      : (uint32_t)n0 * 2u);
+        a_tile0 = __builtin_amdgcn_readfirstlane(((uint32_t)m0 * (uint32_t)K + (uint32_t)k0) * 2u);
+        b_tile0 = __builtin_amdgcn_readfirstlane(
+            B_NK ? ((uint32_t)n0 * (uint32_t)K + (uint32_t)k0) * 2u
+                 : ((uint32_t)k0 * (uint32_t)N + (uint32_t)n0) * 2u);
         b_tile_step = __builtin_amdgcn_readfirstlane(B_NK ? (uint32_t)BK * 2u
                                                           : (uint32_t)BK * (uint32_t)N * 2u);
         const int k_last = K - ((K + BK - 1) / BK - 1) * BK;  // k values of the last tile
@@ -585,12 +592,14 @@ __global__ __launch_bounds__(256, 1) void gemm_sched_kernel(const GemmArgs args)
 
     __shared__ __attribute__((aligned(16))) uint16_t lds[NSLOT * SLOT];
 
-    const int K = args.K;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const GemmOrigin org = gemm_origin(args, BM, BN);
     const int wm0 = (wave & 1) * 128, wn0 = (wave >> 1) * 128;
-    const Ld ld(args, lds, wave, lane, org.m0, org.n0);
+    // this workgroup's K range: its split's chunk (all of K unsplit)
+    const int k0 = org.split * args.k_chunk;
+    const int K = min(args.k_chunk, args.K - k0);
+    const Ld ld(args, lds, wave, lane, org.m0, org.n0, k0);
     // per-lane element offsets of the operand reads inside a slot
     const int a_off = (wm0 + (lane & 15)) * L::A_STRIDE + 8 * (lane >> 4);
     const int b_off = B_NK ? L::A_TILE + (wn0 + (lane & 15)) * L::B_STRIDE + 8 * (lane >> 4)
@@ -715,7 +724,37 @@ __global__ __launch_bounds__(256, 1) void gemm_sched_kernel(const GemmArgs args)
     publish_barrier<0>();
     mfma16_drain();
     static_assert(NSLOT * SLOT * 2 >= NW * 32 * 272, "the staging regions fit the slots");
-    gemm_store16<MB16, NB16>(acc, args, lds, wave, org.m0 + wm0, org.n0 + wn0);
+    if (args.k_splits > 1) {
+        // a split writes its fp32 partial tile to the workspace
+        GemmArgs pa = args;
+        pa.c = args.ws + (long long)org.split * args.M * args.N;
+        pa.out_bf16 = 0;
+        gemm_store16<MB16, NB16>(acc, pa, lds, wave, org.m0 + wm0, org.n0 + wn0);
+    } else {
+        gemm_store16<MB16, NB16>(acc, args, lds, wave, org.m0 + wm0, org.n0 + wn0);
+    }
+}
+
+// C = the sum of the K-split partials ws[s] (fp32 [M][N]) in split order,
+// four consecutive values per thread (M N is a multiple of 8, since N is);
+// fp32 or bf16 (round to nearest even) output.
+template <bool BF16>
+__global__ __launch_bounds__(256) void gemm_split_sum(const float* __restrict__ ws,
+                                                      void* __restrict__ c, long long mn,
+                                                      int splits) {
+    const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+    if (i >= mn / 4) return;
+    g_f32x4 sum = __builtin_nontemporal_load(reinterpret_cast<const g_f32x4*>(ws) + i);
+    for (int s = 1; s < splits; ++s)
+        sum += __builtin_nontemporal_load(reinterpret_cast<const g_f32x4*>(ws + s * mn) + i);
+    if constexpr (BF16) {
+        const float x0 = sum[0], x1 = sum[1], x2 = sum[2], x3 = sum[3];
+        const g_bf16x2 lo = {(__bf16)x0, (__bf16)x1}, hi = {(__bf16)x2, (__bf16)x3};
+        const uint2 w = {__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
+        reinterpret_cast<uint2*>(c)[i] = w;
+    } else {
+        reinterpret_cast<g_f32x4*>(c)[i] = sum;
+    }
 }
 
 template <int BM, int BN, int BK, bool B_NK, int PIPE>
@@ -789,10 +828,16 @@ GemmKernel gemm_variant(const GemmPlan& p) {
 }  // namespace
 
 hipError_t launch_gemm(const GemmPlan& p, const void* a, const void* b, void* c, int M, int N,
-                       int K, int out_bf16, int num_xcds, hipStream_t stream) {
+                       int K, int out_bf16, int num_xcds, float* workspace, hipStream_t stream) {
     const GemmKernel kern = gemm_variant(p);
     if (!kern.fn) return hipErrorInvalidValue;
-    if (gemm_hand_scheduled(p.block_m, p.block_n, p.waves_m, p.waves_n) && K % p.block_k != 0)
+    const bool sched = gemm_hand_scheduled(p.block_m, p.block_n, p.waves_m, p.waves_n);
+    if (sched && K % p.block_k != 0) return hipErrorInvalidValue;
+    const int splits = p.k_splits > 1 ? p.k_splits : 1;
+    if (splits > 1 && (!sched || !workspace || p.k_chunk % p.block_k != 0 ||
+                       (long long)(splits - 1) * p.k_chunk >= K ||
+                       (long long)splits * p.k_chunk < K ||
+                       p.grid != (long long)p.tiles_m * p.tiles_n * splits))
         return hipErrorInvalidValue;
     GemmArgs args;
     args.a = static_cast<const uint16_t*>(a);
@@ -806,8 +851,22 @@ hipError_t launch_gemm(const GemmPlan& p, const void* a, const void* b, void* c,
     args.n_wg = (int)p.grid;
     args.num_xcds = num_xcds;
     args.out_bf16 = out_bf16;
+    args.k_splits = splits;
+    args.k_chunk = splits > 1 ? p.k_chunk : K;
+    args.ws = workspace;
     void* kargs[] = {&args};
-    return hipLaunchKernel(kern.fn, dim3((unsigned)p.grid), dim3(kern.threads), kargs, 0, stream);
+    hipError_t e =
+        hipLaunchKernel(kern.fn, dim3((unsigned)p.grid), dim3(kern.threads), kargs, 0, stream);
+    if (e != hipSuccess || splits == 1) return e;
+    const long long mn = (long long)M * N;
+    const unsigned blocks = (unsigned)((mn / 4 + 255) / 256);
+    if (out_bf16)
+        hipLaunchKernelGGL(gemm_split_sum<true>, dim3(blocks), dim3(256), 0, stream, workspace, c,
+                           mn, splits);
+    else
+        hipLaunchKernelGGL(gemm_split_sum<false>, dim3(blocks), dim3(256), 0, stream, workspace,
+                           c, mn, splits);
+    return hipGetLastError();
 }
 
 bool gemm_resources(const GemmPlan& p, KernelRes* out) {

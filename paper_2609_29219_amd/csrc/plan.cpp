@@ -373,8 +373,14 @@ int gemm_lds_bytes(int bm, int bn, int bk, int b_nk, int pipe) {
 // a tile of LDS, which can cost resident workgroups or rule the largest
 // tiles out.  Lower bounds over the whole product: HBM (A, B read once, C
 // written once) and L2 (A re-read once per tile column, B once per tile row).
+// K split (the same reduction-dimension parallelism as decode's key splits):
+// k_splits workgroups per tile each run k_chunk of K (whole k-tiles, no
+// split empty) into an fp32 partial, and a reduction sums them: the grid
+// grows by k_splits, each workgroup's k-loop shrinks to its chunk, and the
+// partials cost their writes and the reduction's launch and traffic.
 bool plan_gemm_fixed(const attn_device_desc& desc, int M, int N, int K, int b_nk, int bm, int bn,
-                     int bk, int wm, int wn, int pipe, GemmPlan* out, GemmResFn res) {
+                     int bk, int wm, int wn, int pipe, GemmPlan* out, GemmResFn res,
+                     int k_splits) {
     int tile_index = -1;
     for (int i = 0; i < kGemmNumTiles; ++i) {
         const GemmTile& t = kGemmTiles[i];
@@ -384,7 +390,14 @@ bool plan_gemm_fixed(const attn_device_desc& desc, int M, int N, int K, int b_nk
         pipe > kGemmTiles[tile_index].pipe_max)
         return false;
     if (gemm_hand_scheduled(bm, bn, wm, wn) && K % bk != 0) return false;
+    const int n_k_all = (K + bk - 1) / bk;
+    if (k_splits < 1 || (k_splits > 1 && !gemm_hand_scheduled(bm, bn, wm, wn))) return false;
+    const int chunk_tiles = (n_k_all + k_splits - 1) / k_splits;
+    if ((k_splits - 1) * chunk_tiles >= n_k_all) return false;  // a split would be empty
+    if (k_splits > 1 && (long long)k_splits * M * N * 4 > kGemmMaxWorkspaceBytes) return false;
     GemmPlan p;
+    p.k_splits = k_splits;
+    p.k_chunk = k_splits > 1 ? chunk_tiles * bk : K;
     p.block_m = bm;
     p.block_n = bn;
     p.block_k = bk;
@@ -412,7 +425,7 @@ bool plan_gemm_fixed(const attn_device_desc& desc, int M, int N, int K, int b_nk
     if (g < 1) return false;
     p.tiles_m = (M + bm - 1) / bm;
     p.tiles_n = (N + bn - 1) / bn;
-    p.grid = (long long)p.tiles_m * p.tiles_n;
+    p.grid = (long long)p.tiles_m * p.tiles_n * k_splits;
     if (p.grid > 0x7fffffffLL) return false;
     p.wg_per_cu = g;
     // resident workgroups per CU: no more than the grid gives each CU
@@ -449,14 +462,20 @@ bool plan_gemm_fixed(const attn_device_desc& desc, int M, int N, int K, int b_nk
     // (body, exposed latency and bandwidth alike), not the body alone
     round *= gemm_prim_scale(tile_index, b_nk, pipe, gr >= 2.0);
 
-    const int n_k = (K + bk - 1) / bk;
+    const int n_k = chunk_tiles;
     const double store = gr * (double)bm * bn * 4.0 / cu_bw;
     const double rounds = ceil((double)p.grid / (desc.num_cus * gr));
     const double cycles = rounds * (load + heg_for(n_k, round) + store);
     double us = cycles / (desc.clock_ghz * 1e3);
+    // C (fp32) once, or each split's partial written and read back plus C
+    const double c_bytes = (double)M * N * 4.0 * (k_splits > 1 ? 2.0 * k_splits + 1.0 : 1.0);
     const double hbm_us =
-        ((double)M * K * 2.0 + (double)K * N * 2.0 + (double)M * N * 4.0) / desc.hbm_bytes_per_s *
-        1e6;
+        ((double)M * K * 2.0 + (double)K * N * 2.0 + c_bytes) / desc.hbm_bytes_per_s * 1e6;
+    // the reduction: a launch, a dependent memory round trip and its bytes
+    const double reduce_us =
+        k_splits > 1 ? desc.launch_us + desc.hbm_latency_us +
+                           (double)M * N * 4.0 * (k_splits + 1.0) / desc.hbm_bytes_per_s * 1e6
+                     : 0.0;
     const double l2_bytes = (double)M * K * 2.0 * p.tiles_n + (double)K * N * 2.0 * p.tiles_m;
     const double l2_us =
         l2_bytes / (desc.l2_bytes_per_clk_xcd * desc.num_xcds * desc.clock_ghz * 1e9) * 1e6;
@@ -470,7 +489,7 @@ bool plan_gemm_fixed(const attn_device_desc& desc, int M, int N, int K, int b_nk
         us = l2_us;
         bound = "l2";
     }
-    p.modeled_us = us + desc.launch_us;
+    p.modeled_us = us + desc.launch_us + reduce_us;
     p.bound = bound;
     *out = p;
     return true;
@@ -480,13 +499,15 @@ int plan_gemm_all(const attn_device_desc& desc, int M, int N, int K, int b_nk, G
                   int cap, GemmResFn res) {
     int n = 0;
     for (const GemmTile& t : kGemmTiles)
-        for (int pipe = t.pipe_min; pipe <= t.pipe_max; ++pipe) {
-            GemmPlan p;
-            if (!plan_gemm_fixed(desc, M, N, K, b_nk, t.bm, t.bn, t.bk, t.wm, t.wn, pipe, &p, res))
-                continue;
-            if (n < cap) out[n] = p;
-            ++n;
-        }
+        for (int pipe = t.pipe_min; pipe <= t.pipe_max; ++pipe)
+            for (int splits : kGemmKSplits) {
+                GemmPlan p;
+                if (!plan_gemm_fixed(desc, M, N, K, b_nk, t.bm, t.bn, t.bk, t.wm, t.wn, pipe, &p,
+                                     res, splits))
+                    continue;
+                if (n < cap) out[n] = p;
+                ++n;
+            }
     return n;
 }
 
@@ -495,15 +516,17 @@ bool plan_gemm(const attn_device_desc& desc, int M, int N, int K, int b_nk, Gemm
     bool found = false;
     GemmPlan best;
     for (const GemmTile& t : kGemmTiles)
-        for (int pipe = t.pipe_min; pipe <= t.pipe_max; ++pipe) {
-            GemmPlan p;
-            if (!plan_gemm_fixed(desc, M, N, K, b_nk, t.bm, t.bn, t.bk, t.wm, t.wn, pipe, &p, res))
-                continue;
-            if (!found || p.modeled_us < best.modeled_us * (1.0 - 1e-9)) {
-                best = p;
-                found = true;
+        for (int pipe = t.pipe_min; pipe <= t.pipe_max; ++pipe)
+            for (int splits : kGemmKSplits) {
+                GemmPlan p;
+                if (!plan_gemm_fixed(desc, M, N, K, b_nk, t.bm, t.bn, t.bk, t.wm, t.wn, pipe, &p,
+                                     res, splits))
+                    continue;
+                if (!found || p.modeled_us < best.modeled_us * (1.0 - 1e-9)) {
+                    best = p;
+                    found = true;
+                }
             }
-        }
     if (found) *out = best;
     return found;
 }
@@ -511,11 +534,11 @@ bool plan_gemm(const attn_device_desc& desc, int M, int N, int K, int b_nk, Gemm
 int format_gemm_plan(const GemmPlan& p, char* buf, int buflen) {
     return snprintf(buf, buf ? (size_t)buflen : 0,
                     "kind=gemm BLOCK_M=%d BLOCK_N=%d BLOCK_K=%d WAVES_M=%d WAVES_N=%d PIPE=%d "
-                    "b_nk=%d grid=%lld tiles_m=%d tiles_n=%d lds_bytes=%d vgprs=%d wg_per_cu=%d "
-                    "modeled_us=%.3f bound=%s",
-                    p.block_m, p.block_n, p.block_k, p.waves_m, p.waves_n, p.pipe, p.b_nk, p.grid,
-                    p.tiles_m, p.tiles_n, p.lds_bytes, p.vgprs, p.wg_per_cu, p.modeled_us,
-                    p.bound);
+                    "K_SPLITS=%d k_chunk=%d b_nk=%d grid=%lld tiles_m=%d tiles_n=%d lds_bytes=%d "
+                    "vgprs=%d wg_per_cu=%d modeled_us=%.3f bound=%s",
+                    p.block_m, p.block_n, p.block_k, p.waves_m, p.waves_n, p.pipe, p.k_splits,
+                    p.k_chunk, p.b_nk, p.grid, p.tiles_m, p.tiles_n, p.lds_bytes, p.vgprs,
+                    p.wg_per_cu, p.modeled_us, p.bound);
 }
 
 // Query heads per decode workgroup: the largest of 8, 4, 2, 1 dividing the

@@ -307,11 +307,13 @@ def decode_ablation(data: dict, load: bool) -> list:
 GEMM_SHAPES = [(256, 256, 256), (1024, 1024, 1024), (2048, 2048, 2048), (4096, 4096, 4096),
                (8192, 8192, 8192), (16384, 16384, 16384), (16384, 256, 2048), (256, 256, 2048),
                (16384, 256, 16384), (2048, 2048, 16384)]
-GEMM_DOMAINS = ((64, 128, 256), (64, 128, 256), (32, 64), (0, 1, 2, 3))  # BM, BN, BK, pipe
+GEMM_DOMAINS = ((64, 128, 256), (64, 128, 256), (32, 64), (0, 1, 2, 3),
+                (1, 2, 3, 4, 6, 8))  # BM, BN, BK, pipe, K splits
 
 
 def gemm_key(c: dict) -> tuple:
-    return (c["BLOCK_M"], c["BLOCK_N"], c["BLOCK_K"], c["WAVES_M"], c["WAVES_N"], c["PIPE"])
+    return (c["BLOCK_M"], c["BLOCK_N"], c["BLOCK_K"], c["WAVES_M"], c["WAVES_N"], c["PIPE"],
+            c.get("K_SPLITS", 1))
 
 
 def time_gemm(shape, variant, reps=3) -> float:
@@ -326,7 +328,7 @@ def time_gemm(shape, variant, reps=3) -> float:
         time_gemm.cache = (shape, a, b, c)
     _, a, b, c = time_gemm.cache
     iters = 3 if M * N * K > 2 ** 40 else 10
-    os.environ["ATTN_FORCE_GEMM"] = "bm=%d,bn=%d,bk=%d,wm=%d,wn=%d,pipe=%d" % variant
+    os.environ["ATTN_FORCE_GEMM"] = "bm=%d,bn=%d,bk=%d,wm=%d,wn=%d,pipe=%d,splits=%d" % variant
     try:
         for _ in range(3):
             pa.gemm(a, b, c)
@@ -346,13 +348,13 @@ def time_gemm(shape, variant, reps=3) -> float:
 
 
 def gemm_neighbours(pick: tuple, feasible: set) -> list:
-    """Feasible tiles whose BM, BN, BK and pipe are each at most one legal
-    step from the pick's (the paper's local block-size perturbation)."""
+    """Feasible tiles whose BM, BN, BK, pipe and K split are each at most one
+    legal step from the pick's (the paper's local block-size perturbation)."""
     out = []
     for c in feasible:
         steps = [abs(dom.index(x) - dom.index(y))
-                 for dom, x, y in zip(GEMM_DOMAINS, (c[0], c[1], c[2], c[5]),
-                                      (pick[0], pick[1], pick[2], pick[5]))]
+                 for dom, x, y in zip(GEMM_DOMAINS, (c[0], c[1], c[2], c[5], c[6]),
+                                      (pick[0], pick[1], pick[2], pick[5], pick[6]))]
         if max(steps) <= 1 and c != pick:
             out.append(c)
     return sorted(out)
@@ -395,7 +397,7 @@ def main_gemm(a):
     if a.load:
         with open(a.load) as f:
             raw = json.load(f)
-        data = {tuple(map(int, s.split(","))): {tuple(map(int, k.split(","))): t
+        data = {tuple(map(int, s.split(","))): {(tuple(map(int, k.split(","))) + (1,))[:7]: t
                                                for k, t in m.items()} for s, m in raw.items()}
     cands = {shape: pa.gemm_candidates(*shape) for shape in GEMM_SHAPES}
     if not a.load:

@@ -118,7 +118,17 @@ bool check_gemm(const attn_device_desc& desc, const GemmPlan& p, int M, int N, i
     CHECK(p.tiles_m == (M + p.block_m - 1) / p.block_m &&
               p.tiles_n == (N + p.block_n - 1) / p.block_n,
           "tiles %dx%d", p.tiles_m, p.tiles_n);
-    CHECK(p.grid == (long long)p.tiles_m * p.tiles_n, "grid %lld", p.grid);
+    CHECK(p.k_splits >= 1 && (p.k_splits == 1 || scheduled), "k_splits %d", p.k_splits);
+    CHECK(p.grid == (long long)p.tiles_m * p.tiles_n * p.k_splits, "grid %lld", p.grid);
+    if (p.k_splits > 1) {
+        CHECK(p.k_chunk % p.block_k == 0, "k_chunk %d not whole k-tiles", p.k_chunk);
+        CHECK((long long)(p.k_splits - 1) * p.k_chunk < K, "empty last K split");
+        CHECK((long long)p.k_splits * p.k_chunk >= K, "K not covered");
+        CHECK(gemm_workspace_bytes(p, M, N) <= kGemmMaxWorkspaceBytes, "workspace %lld",
+              gemm_workspace_bytes(p, M, N));
+    } else {
+        CHECK(p.k_chunk == K, "unsplit k_chunk %d != K %d", p.k_chunk, K);
+    }
     CHECK(std::isfinite(p.modeled_us) && p.modeled_us > 0.0, "modeled %g", p.modeled_us);
     CHECK(!scheduled || K % p.block_k == 0, "hand-scheduled tile with K %d not whole k-tiles", K);
     return true;

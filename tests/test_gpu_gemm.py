@@ -144,6 +144,48 @@ def test_gemm_hand_scheduled_needs_whole_k_tiles(pa, variant):
     assert e.value.code == pa.ATTN_EINVAL
 
 
+class forced_gemm_split(forced_gemm):
+    def __init__(self, bm, bn, bk, wm, wn, pipe, splits):
+        self.value = f"bm={bm},bn={bn},bk={bk},wm={wm},wn={wn},pipe={pipe},splits={splits}"
+
+
+@pytest.mark.parametrize("splits", [2, 3, 4, 8])
+@pytest.mark.parametrize("variant", [((256, 256, 64, 2, 2), 1), ((256, 256, 32, 2, 2), 3)],
+                         ids=["bk64-pipe1", "bk32-pipe3"])
+def test_gemm_k_splits(pa, variant, splits):
+    # K split into chunks of whole k-tiles, the last one shorter (23 or 46
+    # k-tiles over 2, 3, 4 or 8 splits), ragged M and N, both B layouts and
+    # both outputs; the partials are summed in split order, so repeated calls
+    # agree bit for bit
+    tile, pipe = variant
+    M, N, K = 290, 328, 1472
+    for b_nk in (False, True):
+        a, b = _inputs(M, N, K, b_nk, 4500 + splits)
+        announce(f"attn_gemm {tile} pipe={pipe} splits={splits} b_nk={b_nk}")
+        with forced_gemm_split(*tile, pipe, splits):
+            c = pa.gemm(a.to(DEV), b.to(DEV), b_nk=b_nk)
+            c2 = pa.gemm(a.to(DEV), b.to(DEV), b_nk=b_nk)
+            c16 = pa.gemm(a.to(DEV), b.to(DEV), b_nk=b_nk, out_dtype=torch.bfloat16)
+        torch.cuda.synchronize()
+        want, absc = oracle.gemm(a, b, M, N, K, b_nk=b_nk, with_abs=True)
+        _check(c, want, absc, K, f"split {tile} pipe={pipe} splits={splits} b_nk={b_nk}")
+        assert torch.equal(c, c2), "split GEMM not deterministic"
+        assert torch.equal(c16.cpu(), c.cpu().to(torch.bfloat16)), "bf16 split output"
+
+
+def test_gemm_k_split_refused_when_a_split_would_be_empty(pa):
+    # 2 k-tiles of 64 cannot be split 3 ways (one split would be empty), and
+    # the eight-wave tile has no split form
+    a = torch.zeros((64, 128), dtype=torch.bfloat16, device=DEV)
+    b = torch.zeros((128, 64), dtype=torch.bfloat16, device=DEV)
+    announce("attn_gemm K split refusals")
+    for tile, pipe, splits in (((256, 256, 64, 2, 2), 1, 3), ((256, 256, 64, 2, 4), 1, 2)):
+        with forced_gemm_split(*tile, pipe, splits):
+            with pytest.raises(pa.AttnError) as e:
+                pa.gemm(a, b)
+        assert e.value.code == pa.ATTN_EINVAL
+
+
 def test_gemm_special_values(pa):
     # identity: C = A exactly; zeros: C = 0; a NaN in A spreads only to its row
     M, K = 200, 256
@@ -174,7 +216,7 @@ def test_gemm_deterministic_and_stream_ordered(pa):
 
 
 LARGE = [(4096, 4096, 4096, False), (16384, 256, 2048, True), (256, 256, 16384, False),
-         (2048, 8192, 1024, True)]
+         (2048, 8192, 1024, True), (2048, 2048, 16384, False), (16384, 256, 16384, True)]
 
 
 @pytest.mark.parametrize("shape", LARGE, ids=[str(s) for s in LARGE])

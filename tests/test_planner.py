@@ -249,8 +249,34 @@ def test_gemm_plan_is_the_argmin_of_its_candidates(shape, b_nk):
     assert abs(p["modeled_us"] - best) <= 1e-3 * best
     for c in cands:
         assert c["lds_bytes"] <= desc.lds_bytes_per_cu
-        assert c["grid"] == -(-M // c["BLOCK_M"]) * -(-N // c["BLOCK_N"])
+        splits = c["K_SPLITS"]
+        assert c["grid"] == -(-M // c["BLOCK_M"]) * -(-N // c["BLOCK_N"]) * splits
         assert c["b_nk"] == int(b_nk)
+        if splits > 1:
+            # hand-scheduled tiles only, whole k-tiles per split, none empty
+            assert (c["BLOCK_M"], c["BLOCK_N"], c["WAVES_M"], c["WAVES_N"]) == (256, 256, 2, 2)
+            assert c["k_chunk"] % c["BLOCK_K"] == 0
+            assert (splits - 1) * c["k_chunk"] < K <= splits * c["k_chunk"]
+        else:
+            assert c["k_chunk"] == K
+
+
+def test_gemm_k_split_model():
+    # a K split pays partial traffic and a reduction: the planner never splits
+    # a GEMM that already fills the CUs, and does split one with few output
+    # tiles and a long K, whose split candidates it then ranks above the
+    # unsplit one of the same tile
+    desc = spec()
+    big = pa.parse_plan(pa.gemm_plan(8192, 8192, 8192, desc=desc))
+    assert big["K_SPLITS"] == 1
+    thin = pa.parse_plan(pa.gemm_plan(2048, 2048, 16384, desc=desc))
+    assert thin["K_SPLITS"] > 1
+    same_tile = [c for c in pa.gemm_candidates(2048, 2048, 16384, desc=desc)
+                 if (c["BLOCK_M"], c["BLOCK_N"], c["BLOCK_K"], c["WAVES_M"], c["WAVES_N"],
+                     c["PIPE"]) == (thin["BLOCK_M"], thin["BLOCK_N"], thin["BLOCK_K"],
+                                    thin["WAVES_M"], thin["WAVES_N"], thin["PIPE"])]
+    unsplit = [c for c in same_tile if c["K_SPLITS"] == 1]
+    assert unsplit and unsplit[0]["modeled_us"] > thin["modeled_us"]
 
 
 def test_gemm_double_buffer_trade_off():
@@ -261,7 +287,9 @@ def test_gemm_double_buffer_trade_off():
     cands = pa.gemm_candidates(8192, 8192, 8192, False, desc=desc, analytic_only=True)
     by_tile = {}
     for c in cands:
-        by_tile.setdefault((c["BLOCK_M"], c["BLOCK_N"], c["BLOCK_K"]), {})[c["PIPE"]] = c
+        if c["K_SPLITS"] == 1:
+            by_tile.setdefault((c["BLOCK_M"], c["BLOCK_N"], c["BLOCK_K"], c["WAVES_M"],
+                                c["WAVES_N"]), {})[c["PIPE"]] = c
     for tile, pair in by_tile.items():
         if 0 in pair and 1 in pair:
             assert pair[1]["lds_bytes"] == 2 * pair[0]["lds_bytes"]
