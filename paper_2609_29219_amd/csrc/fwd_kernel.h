@@ -28,6 +28,18 @@
 // The output accumulator holds one query per lane, so the online-softmax
 // rescale is one per-lane scalar.
 //
+// Row sums.  The normaliser (the running sum of the bf16 probabilities) is
+// accumulated on the matrix core too, with one v_mfma_f32_16x16x32_bf16 per
+// 16-key step: its B operand is the PV MFMA's probability register read as a
+// 32 x 16 matrix (lane l holds k-group l/16, column l%16), so k-groups 0 and 2
+// are the 16 keys of query c = l%16 and k-groups 1 and 3 those of query c+16.
+// A is a constant 0/1 selector with A[i][k] = 1 iff (k/8)%2 == (i/4)%2, so the
+// output rows 4g..4g+3 that lane l holds (g = l/16) sum the keys of query
+// c + 16*(g%2) = l%32: each lane gets the row sum of its own query, in the
+// same lane as its output accumulator, with no exchange between lanes.  This
+// replaces four VALU instructions per pair of probabilities; the variants
+// already at the 256-register limit keep the VALU sum (fwd_mfma_row_sum).
+//
 // LDS layout (64 banks of 4 bytes).  K rows are padded to D+8 bf16, so
 // consecutive rows start 4 banks apart and the 16 lanes a ds_read_b128
 // serves per cycle cover all 64 banks; V rows are padded to D+32 bf16, so the
@@ -78,6 +90,7 @@ namespace attn {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x8 __attribute__((ext_vector_type(8)));
@@ -120,13 +133,25 @@ __device__ __forceinline__ s16x4 lds_read_tr(const uint16_t* p) {
 
 constexpr int fwd_slots(int pipe) { return pipe == 0 ? 1 : 2; }
 
-// Software-pipeline lag (0, 1 or 2 slots) between the exponentials of a
+// Row sums on the matrix core (8 more registers per wave: the selector and
+// the accumulator) everywhere but in the d = 128 kernels that would then
+// spill: 128-key tiles, and the four-wave software pipeline.
+constexpr bool fwd_mfma_row_sum(int d, int bn, int nw, int pipe) {
+    return !(d == 128 && (bn == 128 || (nw == 4 && pipe == 3)));
+}
+
+// Entries of the software pipeline's LDS operand ring (operands are fetched
+// PF - 1 MFMAs ahead): two in the causal kernels, which need the registers
+// for their masks, three elsewhere (more measured no faster).
+constexpr int fwd_operand_ring(bool causal) { return causal ? 2 : 3; }
+
+// Software-pipeline lag (0 to max_lag slots) between the exponentials of a
 // probability pair and its rounding: the largest for which every pair is
 // still rounded in a slot before the first PV MFMA of its 16-key step (the
 // pair's work follows the slot's MFMA in program order); -1 if even lag 0
 // violates that.
-constexpr int fwd_pair_lag(int npair, int exp_slots, int ns, int cb) {
-    for (int lag = 2; lag >= 0; --lag) {
+constexpr int fwd_pair_lag(int npair, int exp_slots, int ns, int cb, int max_lag = 2) {
+    for (int lag = max_lag; lag >= 0; --lag) {
         bool ok = true;
         for (int pp = 0; pp < npair; ++pp)
             if (pp * exp_slots / npair + lag >= ns + (pp / 4) * cb) ok = false;
@@ -408,7 +433,22 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
 
     // ---- online-softmax state (one query row per lane) --------------------
     float m_i = -INFINITY;  // running max of scaled scores, log2 domain
-    float l_i = 0.f;        // running sum of bf16-rounded probabilities (this half's keys)
+    // Running sum of the row's bf16 probabilities: on the matrix core (all
+    // four registers of lsum hold it; lsum += sel * P^T per 16-key step, sel
+    // the constant 0/1 selector described at the top of the file), or on the
+    // VALU in l_i (this lane's half of the keys).
+    constexpr bool MSUM = fwd_mfma_row_sum(D, BN, NW, PIPE);
+    float l_i = 0.f;
+    f32x4 lsum = {0.f, 0.f, 0.f, 0.f};
+    bf16x8 sel;
+    if constexpr (MSUM) {
+        const __bf16 v = ((lane >> 4) & 1) == ((lane >> 2) & 1) ? (__bf16)1.0f : (__bf16)0.0f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sel[e] = v;
+    }
+    auto row_sum = [&](const bf16x8& p) __attribute__((always_inline)) {
+        if constexpr (MSUM) lsum = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel, p, lsum, 0, 0, 0);
+    };
     f32x16 oacc[CB];
 #pragma unroll
     for (int cb = 0; cb < CB; ++cb)
@@ -465,7 +505,10 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
         if (__any(move)) {
             const float m_new = move ? tmax : m_i;
             const float alpha = __builtin_amdgcn_exp2f(m_i - m_new);  // 0 when m_i = -inf
-            l_i *= alpha;
+            if constexpr (MSUM)
+                lsum *= alpha;
+            else
+                l_i *= alpha;
 #pragma unroll
             for (int cb = 0; cb < CB; ++cb)
 #pragma unroll
@@ -477,20 +520,23 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     auto softmax_stats = [&](f32x16 (&s)[KB], int t, auto mask_tag) __attribute__((always_inline)) -> float {
         return update_ref(tile_max(s, t, mask_tag));
     };
-    // bf16 probabilities of a tile (VALU only) and their sum.  The sum is
-    // taken over the rounded values (bf16 -> fp32 is a shift or a mask), so
-    // the weights applied to V sum exactly to the normaliser: the output is a
-    // convex combination of V rows up to fp32 rounding.  Masked scores are
-    // -inf and the scale is > 0, so they give exactly 0.
+    // bf16 probabilities of a tile (VALU only).  The normaliser sums these
+    // rounded values (row_sum next to the PV MFMAs that apply them, or here
+    // on the VALU, where bf16 -> fp32 is a shift or a mask), so the weights
+    // applied to V sum exactly to the normaliser: the output is a convex
+    // combination of V rows up to fp32 rounding.  Masked scores are -inf and
+    // the scale is > 0, so they give exactly 0.
     auto rounded_pair = [&](float x0, float x1, bf16x8& dst, int e, float& r0, float& r1)
         __attribute__((always_inline)) {
         // one packed conversion; both halves are read back from it
         const bf16x2 pk = {(__bf16)x0, (__bf16)x1};
         dst[e] = pk[0];
         dst[e + 1] = pk[1];
-        const uint32_t w = __builtin_bit_cast(uint32_t, pk);
-        r0 += __uint_as_float(w << 16);
-        r1 += __uint_as_float(w & 0xffff0000u);
+        if constexpr (!MSUM) {
+            const uint32_t w = __builtin_bit_cast(uint32_t, pk);
+            r0 += __uint_as_float(w << 16);
+            r1 += __uint_as_float(w & 0xffff0000u);
+        }
     };
     auto probs = [&](const f32x16 (&s)[KB], float m_ref, bf16x8 (&pb)[KB][2])
         __attribute__((always_inline)) {
@@ -505,10 +551,11 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
                         __builtin_amdgcn_exp2f(fmaf(s[kb][8 * h2 + e], scale_log2, -m_ref)),
                         __builtin_amdgcn_exp2f(fmaf(s[kb][8 * h2 + e + 1], scale_log2, -m_ref)),
                         pb[kb][h2], e, rs0, rs1);
-        l_i += rs0 + rs1;
+        if constexpr (!MSUM) l_i += rs0 + rs1;
     };
 
-    // O^T += V^T P^T in groups of 8 keys; V^T operands by transposed reads.
+    // O^T += V^T P^T in steps of 16 keys (and the row sums of P); V^T
+    // operands by transposed reads.
     const int tr_row = (lane & 15) >> 2;                         // + k0
     const int tr_col = ((lane >> 4) & 1) * 16 + 4 * (lane & 3);  // + cb*32
     auto pv = [&](const uint16_t* vl, const bf16x8 (&pb)[KB][2]) __attribute__((always_inline)) {
@@ -516,6 +563,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
         for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
             for (int h2 = 0; h2 < 2; ++h2) {
+                row_sum(pb[kb][h2]);
                 const uint16_t* p =
                     vl + (kb * 32 + 16 * hh + 8 * h2 + tr_row) * L::V_STRIDE + tr_col;
 #pragma unroll
@@ -546,19 +594,23 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
         constexpr int NS = HAS_S ? KB * KD : 0;  // MFMAs of S(t+1)
         constexpr int NPV = KB * 2 * CB;          // MFMAs of PV(t)
         constexpr int NM = NS + NPV;
-        constexpr int PF = 3;  // ring entries (fits 256 VGPRs also in the causal kernels)
+        constexpr int PF = fwd_operand_ring(CAUSAL);
         constexpr int NPAIR = KB * 8;                    // pairs of probabilities per lane
         constexpr int EXP_SLOTS = HAS_S ? NS + NPV / 2 : 0;  // slots carrying exponentials
         constexpr int MAX0 = EXP_SLOTS + 1;              // first slot carrying the next max
         constexpr int NMAXV = HAS_S ? KB * 16 : 0;      // scores of tile t+1 per lane
         static_assert(!HAS_S || MAX0 < NM, "too few MFMAs to carry the softmax");
         // The exponentials of pair pp (16-key step pp / 4) are taken in slot
-        // pp * EXP_SLOTS / NPAIR and rounded and summed LAG slots later, so the
-        // rounding does not wait on a just-issued exponential; the rounded
-        // pair must still precede the first PV MFMA of its step, in slot
-        // NS + (pp / 4) * CB.
-        // (not with four waves: their 64-key kernel then spills)
-        constexpr int LAG = HAS_S && NW == 8 ? fwd_pair_lag(NPAIR, EXP_SLOTS, NS, CB) : 0;
+        // pp * EXP_SLOTS / NPAIR and rounded (and, with VALU row sums,
+        // summed) LAG slots later, so the rounding does not wait on a
+        // just-issued exponential; the rounded pair must still precede the
+        // first PV MFMA of its step, in slot NS + (pp / 4) * CB.
+        // (not with four waves: their 64-key kernel then spills).  At most one
+        // slot where the rounding is a single conversion (row sums on the
+        // matrix core) and the kernel is not causal; two elsewhere (measured).
+        constexpr int LAG = HAS_S && NW == 8
+                                ? fwd_pair_lag(NPAIR, EXP_SLOTS, NS, CB, MSUM && !CAUSAL ? 1 : 2)
+                                : 0;
         static_assert(!HAS_S || fwd_pair_lag(NPAIR, EXP_SLOTS, NS, CB) >= 0,
                       "probabilities must precede their PV MFMAs");
         auto fetch = [&](int i) __attribute__((always_inline)) -> bf16x8 {
@@ -606,7 +658,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
         // slot i - 1 consumed (an MFMA still reading its operands must not see
         // them overwritten), so operands arrive PF - 1 slots early.  Each slot
         // is its own scheduling region (sched_barrier), and an empty asm that
-        // reads and writes the running sums and max keeps the pure arithmetic
+        // reads and writes the running max (and sums) keeps the pure arithmetic
         // of the slot from drifting to the end of the tile.
         bf16x8 fr[PF];
         static_for<0, PF - 1>([&](auto ic) __attribute__((always_inline)) {
@@ -623,6 +675,8 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
                 constexpr int j = i - NS, kb = j / (2 * CB), h2 = (j / CB) % 2, cb = j % CB;
                 oacc[cb] =
                     __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kb][h2], oacc[cb], 0, 0, 0);
+                // the step's row sums right behind its first PV MFMA (same B)
+                if constexpr (cb == 0) row_sum(pb[kb][h2]);
             }
             if constexpr (HAS_S) {
                 static_for<0, NPAIR>([&](auto pc) __attribute__((always_inline)) {
@@ -646,10 +700,11 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
                     }
                 });
             }
-            if constexpr (HAS_S) asm volatile("" : "+v"(rs0), "+v"(rs1), "+v"(mx));
+            if constexpr (HAS_S && MSUM) asm volatile("" : "+v"(mx));
+            if constexpr (HAS_S && !MSUM) asm volatile("" : "+v"(rs0), "+v"(rs1), "+v"(mx));
             __builtin_amdgcn_sched_barrier(0);
         });
-        l_i += rs0 + rs1;
+        if constexpr (!MSUM) l_i += rs0 + rs1;
         return HAS_S ? half_swap_max(mx) : -INFINITY;
     };
 
@@ -820,7 +875,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     // the reference m_i is in log2 units and includes the scale)
     // With split keys the row's unnormalised partials (m_i, l, O) go to the
     // workspace instead (the split combine normalises).
-    const float l_row = half_swap_sum(l_i);
+    const float l_row = MSUM ? lsum[0] : half_swap_sum(l_i);
     // (not with the ping-pong schedule, which has no registers to spare)
     const bool partial = PIPE != 2 && kv_splits > 1;
     const float inv = partial ? 1.f : 1.f / l_row;
