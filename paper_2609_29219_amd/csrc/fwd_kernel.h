@@ -9,8 +9,9 @@
 // (A = 32 keys x 16 dims read from LDS, B = 16 dims x 32 queries held in
 // VGPRs).  The 32x32 accumulator puts one query column in each lane
 // (lane & 31) and 16 keys of it in that lane's 16 registers (the other 16
-// keys sit in lane ^ 32).  Row max and row sum are in-lane reductions plus
-// one exchange between the wave halves (v_permlane32_swap).
+// keys sit in lane ^ 32).  The row max is an in-lane reduction plus one
+// exchange between the wave halves (v_permlane32_swap); the row sum is taken
+// by the matrix core (below).
 //
 // Key permutation.  Accumulator register r of lane half h holds MFMA row
 // 8*(r/4) + 4*h + r%4.  K rows are written to LDS permuted inside each
@@ -142,7 +143,8 @@ constexpr bool fwd_mfma_row_sum(int d, int bn, int nw, int pipe) {
 
 // Entries of the software pipeline's LDS operand ring (operands are fetched
 // PF - 1 MFMAs ahead): two in the causal kernels, which need the registers
-// for their masks, three elsewhere (more measured no faster).
+// for their masks and the row-sum MFMA (and measured as fast with two),
+// three elsewhere (more measured no faster).
 constexpr int fwd_operand_ring(bool causal) { return causal ? 2 : 3; }
 
 // Software-pipeline lag (0 to max_lag slots) between the exponentials of a
@@ -528,7 +530,7 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
     // the scale is > 0, so they give exactly 0.
     auto rounded_pair = [&](float x0, float x1, bf16x8& dst, int e, float& r0, float& r1)
         __attribute__((always_inline)) {
-        // one packed conversion; both halves are read back from it
+        // one packed conversion (the VALU sum reads both halves back from it)
         const bf16x2 pk = {(__bf16)x0, (__bf16)x1};
         dst[e] = pk[0];
         dst[e + 1] = pk[1];
