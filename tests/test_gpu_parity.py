@@ -141,6 +141,32 @@ def test_fwd_special_cases(pa):
     np.testing.assert_allclose(o[0, 1, 17], vn[0, 1, star], atol=1e-5, rtol=0)
 
 
+@pytest.mark.parametrize("variant", VARIANTS, ids=[f"bn{a}_w{b}_pipe{c}" for a, b, c in VARIANTS])
+@pytest.mark.parametrize("d", [64, 128])
+def test_fwd_exact_normaliser_every_kernel_variant(pa, variant, d):
+    """The weights applied to V sum to the normaliser (both are sums of the
+    same bf16-rounded probabilities), so identical V rows come back exactly and
+    a column of ones stays 1, in every kernel variant: those whose row sums run
+    on the matrix core and those that keep them on the VALU.  Ragged key and
+    query counts, causal and not."""
+    bn, waves, pipe = variant
+    B, H, Sq, Skv = 1, 2, 137, 203
+    q = _rand4(B, H, Sq, d, 500 + d)
+    k = _rand4(B, H, Skv, d, 501 + d)
+    row = random_bf16((d,), 502 + d)
+    vrow = row.expand(B, H, Skv, d).contiguous()
+    v1 = _rand4(B, H, Skv, d, 503 + d)
+    v1[..., 3] = 1.0
+    with forced_plan(bn, waves, pipe):
+        for causal in (False, True):
+            o = pa.attn_fwd(q.to(DEV), k.to(DEV), vrow.to(DEV), causal=causal)
+            o = o.cpu().double().numpy()
+            np.testing.assert_allclose(o, np.broadcast_to(row.double().numpy(), o.shape),
+                                       atol=2e-6, rtol=1e-6)
+            o = pa.attn_fwd(q.to(DEV), k.to(DEV), v1.to(DEV), causal=causal).cpu().double().numpy()
+            np.testing.assert_allclose(o[..., 3], 1.0, atol=1e-6, rtol=0)
+
+
 def test_fwd_nan_poisoned_output_fully_written(pa):
     B, H, Sq, Skv, d = 2, 3, 333, 200, 128
     q, k, v = _rand4(B, H, Sq, d, 500), _rand4(B, H, Skv, d, 501), _rand4(B, H, Skv, d, 502)
