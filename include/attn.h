@@ -101,7 +101,9 @@ int attn_fwd_ex(const void* q, const void* k, const void* v, void* o, float* lse
 
 /*
  * Single-query attention with the KV sequence split across workgroups
- * (Flash Decode), then a log-sum-exp combine of the partial results.
+ * (Flash Decode), then a log-sum-exp combine of the partial results (with a
+ * single split the partial kernel writes o itself: the combine would be the
+ * identity).
  *   q: bf16 [B][H][d]      k, v: bf16 [B][H][Skv][d]      o: fp32 [B][H][d]
  *   scale is fixed to (float)(1/sqrt(d)).
  *   n_splits <= 0: the planner chooses the split count from the device's

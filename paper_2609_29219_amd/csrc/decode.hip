@@ -16,7 +16,10 @@
 // any use.  The q.k dot product is reduced across the G lanes with DPP.
 // At the end the groups of the workgroup merge through LDS, and the
 // workgroup writes (m, l, o[d]) of its split, unnormalised, to the
-// workspace (m in the base-2 domain).
+// workspace (m in the base-2 domain).  With a single split the combine would
+// be the identity (one weight 2^0 = 1), so the partial kernels then write the
+// normalised output o / l, and the log-sum-exp, themselves: the same values,
+// one launch less.
 #include "common.h"
 
 namespace attn {
@@ -36,6 +39,25 @@ __device__ __forceinline__ float group_sum(float x) {
     return x;
 }
 
+// The merged (m, l, o[c]) of row `out` (row * n_splits + split): into the
+// workspace, or, with a single split (o_final set; then out is the row), as
+// the final output o / l and the row's log-sum-exp (natural log).
+template <int D>
+__device__ __forceinline__ void store_partial(long long out, int c, float M, float L, float acc,
+                                              float* ws_m, float* ws_l, float* ws_o,
+                                              float* o_final, float* lse_final) {
+    if (o_final) {
+        o_final[out * D + c] = acc / L;
+        if (lse_final && c == 0) lse_final[out] = (M + __builtin_log2f(L)) * 0.69314718055994531f;
+        return;
+    }
+    ws_o[out * D + c] = acc;
+    if (c == 0) {
+        ws_m[out] = M;
+        ws_l[out] = L;
+    }
+}
+
 // GQ query heads that share one key/value head (grouped-query attention) run
 // in the same workgroup, so each K and V row is read from memory once for
 // all of them: a lane keeps GQ query slices, GQ online-softmax states and GQ
@@ -44,7 +66,8 @@ template <int D, int NT, int U, int GQ>
 __global__ __launch_bounds__(NT) void decode_partial_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, float* __restrict__ ws_m, float* __restrict__ ws_l,
-    float* __restrict__ ws_o, int Skv, int chunk, int n_splits, int group, float scale_log2) {
+    float* __restrict__ ws_o, float* __restrict__ o_final, float* __restrict__ lse_final, int Skv,
+    int chunk, int n_splits, int group, float scale_log2) {
     constexpr int G = D / 8;      // lanes per key
     constexpr int NG = NT / G;    // lane groups (keys per step) in the workgroup
     const int tid = threadIdx.x;
@@ -149,11 +172,7 @@ __global__ __launch_bounds__(NT) void decode_partial_kernel(
                 L = fmaf(w, sl[q], L);
                 acc = fmaf(w, so[q][c], acc);
             }
-            ws_o[out * D + c] = acc;
-            if (c == 0) {
-                ws_m[out] = M;
-                ws_l[out] = L;
-            }
+            store_partial<D>(out, c, M, L, acc, ws_m, ws_l, ws_o, o_final, lse_final);
         }
         __syncthreads();  // the LDS merge buffers are reused by the next query
     }
@@ -179,7 +198,8 @@ __global__ __launch_bounds__(NT) void decode_partial_kernel(
 //     swaps), probabilities rounded to bf16 and the sum l over the rounded
 //     values (so the output is an exact convex combination of V rows);
 //   * the four waves merge through LDS and write the same unnormalised
-//     (m, l, o[d]) partials per (query head, split) as the kernel above.
+//     (m, l, o[d]) partials per (query head, split) as the kernel above (or,
+//     with a single split, the final output).
 // Every memory operation is an ordinary load or LDS access the compiler
 // tracks; latency is hidden by occupancy (16 KiB in flight per wave).
 typedef __bf16 gq_bf16x8 __attribute__((ext_vector_type(8)));
@@ -209,8 +229,9 @@ template <int D>
 __global__ __launch_bounds__(kGqaWaves * 64) void gqa_decode_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, float* __restrict__ ws_m, float* __restrict__ ws_l,
-    float* __restrict__ ws_o, int Hq, int Hkv, int Skv, int chunk, int n_splits, int q_blocks,
-    int n_wg, int num_xcds, float scale_log2) {
+    float* __restrict__ ws_o, float* __restrict__ o_final, float* __restrict__ lse_final, int Hq,
+    int Hkv, int Skv, int chunk, int n_splits, int q_blocks, int n_wg, int num_xcds,
+    float scale_log2) {
     constexpr int KS = D / 32;        // MFMA k-steps over the head dimension
     constexpr int DB = D / 16;        // 16-dim blocks of O^T
     constexpr int VST = D + 32;       // bf16 per padded V row in LDS
@@ -368,11 +389,7 @@ __global__ __launch_bounds__(kGqaWaves * 64) void gqa_decode_kernel(
             acc = fmaf(wt, so[(w * D + c) * 16 + q], acc);
         }
         const long long out = (b * Hq + q_first + q) * n_splits + split;
-        ws_o[out * D + c] = acc;
-        if (c == 0) {
-            ws_m[out] = M;
-            ws_l[out] = L;
-        }
+        store_partial<D>(out, c, M, L, acc, ws_m, ws_l, ws_o, o_final, lse_final);
     }
 }
 
@@ -428,15 +445,15 @@ hipError_t launch_split_combine(int d, const float* ws_m, const float* ws_l, con
 template <int D, int GQ>
 static hipError_t launch_partial(const DecodePlan& p, const void* q, const void* k,
                                  const void* v, float* ws_m, float* ws_l, float* ws_o,
-                                 long long BHq, int Skv, int group, float scale_log2,
-                                 hipStream_t st) {
+                                 float* o_final, float* lse_final, long long BHq, int Skv,
+                                 int group, float scale_log2, hipStream_t st) {
     // fewer keys in flight per lane group when each key serves many queries
     constexpr int U = GQ >= 4 ? 4 : kDecodeUnroll;
     hipLaunchKernelGGL((decode_partial_kernel<D, kDecodeThreads, U, GQ>),
                        dim3((unsigned)(BHq / GQ * p.n_splits)), dim3(kDecodeThreads), 0, st,
                        static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
-                       static_cast<const uint16_t*>(v), ws_m, ws_l, ws_o, Skv, p.chunk,
-                       p.n_splits, group, scale_log2);
+                       static_cast<const uint16_t*>(v), ws_m, ws_l, ws_o, o_final, lse_final,
+                       Skv, p.chunk, p.n_splits, group, scale_log2);
     return hipGetLastError();
 }
 
@@ -450,24 +467,29 @@ static hipError_t launch_decode_d(const DecodePlan& p, const void* q, const void
     float* ws_m = ws;
     float* ws_l = ws + BHq * p.n_splits;
     float* ws_o = ws + 2 * BHq * p.n_splits;
+    // a single split writes the output directly (no combine launch)
+    const bool direct = p.n_splits == 1;
+    float* const o_final = direct ? o : nullptr;
+    float* const lse_final = direct ? lse : nullptr;
     hipError_t e = hipErrorInvalidValue;
     if (p.mfma) {
         if (p.grid > 0x7fffffffLL || p.q_blocks != (group + 15) / 16) return hipErrorInvalidValue;
         hipLaunchKernelGGL((gqa_decode_kernel<D>), dim3((unsigned)p.grid), dim3(kGqaWaves * 64), 0,
                            st, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
-                           static_cast<const uint16_t*>(v), ws_m, ws_l, ws_o, Hq, Hkv, Skv,
-                           p.chunk, p.n_splits, p.q_blocks, (int)p.grid, num_xcds, scale_log2);
+                           static_cast<const uint16_t*>(v), ws_m, ws_l, ws_o, o_final, lse_final,
+                           Hq, Hkv, Skv, p.chunk, p.n_splits, p.q_blocks, (int)p.grid, num_xcds,
+                           scale_log2);
         e = hipGetLastError();
-        if (e != hipSuccess) return e;
+        if (e != hipSuccess || direct) return e;
         return launch_split_combine(D, ws_m, ws_l, ws_o, o, 0, lse, BHq, p.n_splits, st);
     }
     switch (decode_heads_per_wg(group)) {
-        case 8: e = launch_partial<D, 8>(p, q, k, v, ws_m, ws_l, ws_o, BHq, Skv, group, scale_log2, st); break;
-        case 4: e = launch_partial<D, 4>(p, q, k, v, ws_m, ws_l, ws_o, BHq, Skv, group, scale_log2, st); break;
-        case 2: e = launch_partial<D, 2>(p, q, k, v, ws_m, ws_l, ws_o, BHq, Skv, group, scale_log2, st); break;
-        default: e = launch_partial<D, 1>(p, q, k, v, ws_m, ws_l, ws_o, BHq, Skv, group, scale_log2, st);
+        case 8: e = launch_partial<D, 8>(p, q, k, v, ws_m, ws_l, ws_o, o_final, lse_final, BHq, Skv, group, scale_log2, st); break;
+        case 4: e = launch_partial<D, 4>(p, q, k, v, ws_m, ws_l, ws_o, o_final, lse_final, BHq, Skv, group, scale_log2, st); break;
+        case 2: e = launch_partial<D, 2>(p, q, k, v, ws_m, ws_l, ws_o, o_final, lse_final, BHq, Skv, group, scale_log2, st); break;
+        default: e = launch_partial<D, 1>(p, q, k, v, ws_m, ws_l, ws_o, o_final, lse_final, BHq, Skv, group, scale_log2, st);
     }
-    if (e != hipSuccess) return e;
+    if (e != hipSuccess || direct) return e;
     return launch_split_combine(D, ws_m, ws_l, ws_o, o, 0, lse, BHq, p.n_splits, st);
 }
 

@@ -590,9 +590,12 @@ bool plan_decode(const attn_device_desc& desc, int B, int Hq, int Hkv, int Skv, 
         const double steps = ceil((double)chunk / step_keys);
         const double stream_us = per_cu * wg_bytes / cu_bw * 1e6;
         const double merge_us = ceil(per_cu / resident) * 1.0;  // LDS merge + write, ~1 us
+        // the split combine (a single split writes the output itself)
         const double combine_bytes = (double)BHq * n_eff * (d + 2) * 4.0 + BHq * d * 4.0;
-        const double combine_us = desc.launch_us + 2.0 * desc.hbm_latency_us +
-                                  combine_bytes / desc.hbm_bytes_per_s * 1e6 + n_eff * 0.01;
+        const double combine_us = n_eff > 1 ? desc.launch_us + 2.0 * desc.hbm_latency_us +
+                                                  combine_bytes / desc.hbm_bytes_per_s * 1e6 +
+                                                  n_eff * 0.01
+                                            : 0.0;
         p->d = d;
         p->n_splits = n_eff;
         p->chunk = chunk;
