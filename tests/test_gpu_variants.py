@@ -156,6 +156,8 @@ DECODE_GQA = [  # B, Hq, Hkv, Skv, d, n_splits  (group >= 4: the matrix-core ker
     (3, 8, 2, 33, 128, 0),      # fewer keys than one 32-key step per wave
     (2, 20, 4, 1, 64, 0),       # a single key
     (1, 64, 8, 65536, 128, 0),  # long context, group 8
+    (2, 8, 2, 1000, 128, 1),    # one split: the matrix-core kernel writes o and lse itself
+    (3, 6, 2, 777, 64, 1),      # one split, the VALU kernel (group 3)
 ]
 
 
