@@ -243,16 +243,20 @@ bool plan_fwd_fixed(const attn_device_desc& desc, int B, int H, int Sq, int Skv,
             const int kv_end = std::min(Skv, last_q + (Skv - Sq) + 1);
             return (kv_end + bn - 1) / bn;
         };
+        // workgroups resident per CU: no more than the grid gives each CU
+        // (a grid of one workgroup per CU runs its tiles alone on the CU)
+        const int g_eff = (int)std::min<double>(wg, ceil((double)p.grid / desc.num_cus));
+        const double tile_c = g_eff == wg ? tile : tile_cost(g_eff, nullptr, nullptr);
         double sum = 0.0, longest = 0.0;
         const int units = (p.n_qtiles + 1) / 2;
         for (int u = 0; u < units; ++u) {
             const int heavy = p.n_qtiles - 1 - u;
-            double t = load_q + heg_for(tiles_of(heavy), tile);
-            if (heavy != u) t += load_q + heg_for(tiles_of(u), tile);
+            double t = load_q + heg_for(tiles_of(heavy), tile_c);
+            if (heavy != u) t += load_q + heg_for(tiles_of(u), tile_c);
             sum += t;
             longest = std::max(longest, t);
         }
-        const double rounds = ceil((double)p.grid / slots);
+        const double rounds = ceil((double)p.grid / ((double)desc.num_cus * g_eff));
         cycles = std::max(rounds * sum / units, longest);
     }
     double us = cycles / (desc.clock_ghz * 1e3);
