@@ -103,6 +103,28 @@ def test_causal_models_about_half_the_work():
     assert 0.35 * nc < c < 0.8 * nc
 
 
+def test_causal_residency_follows_the_grid():
+    """A causal grid of one workgroup per CU runs each workgroup alone on its
+    CU, whatever the kernel's footprint would allow: doubling it while it
+    still fits one round of that footprint doubles the work resident on
+    each CU and must cost time (the model used to charge both grids at the
+    footprint's residency, the same time)."""
+    d = spec()
+    cands = lambda B: {(c["BLOCK_N"], c["WAVES"], c["PIPE"]): c
+                       for c in pa.fwd_candidates(B, 16, 4096, 4096, 64, True, desc=d)
+                       if c["KV_SPLITS"] == 1}
+    one, two = cands(2), cands(4)
+    checked = 0
+    for key, c in one.items():
+        if key not in two or c["wg_per_cu"] < 2 or c["grid"] > d.num_cus:
+            continue
+        if two[key]["grid"] > d.num_cus * c["wg_per_cu"]:
+            continue
+        assert two[key]["modeled_us"] > 1.4 * c["modeled_us"], key
+        checked += 1
+    assert checked > 0
+
+
 def test_modeled_time_grows_with_work():
     d = spec()
     t = [plan(d, pa.KIND_FWD, 1, h, 4096, 4096, 128)["modeled_us"] for h in (8, 32, 128)]
