@@ -831,10 +831,14 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
         }
         tile_barrier();  // slot 0 takes K_2 at the end of iteration 0
 
-        // Iteration t.  Its S(t+1) also runs on the last tile, against a stale
-        // but finite K slot, and on a wave's first inactive tile; those scores
-        // are never used.  Keeping S(t+1) unconditional leaves one body per
-        // masking mode.
+        // Iteration t of the loop: PV(t) and S(t+1), up to the tile before the
+        // wave's last active one.  The last active tile runs once after the
+        // loop, without scores of a next tile (which would never be used: on
+        // the last tile they would come from a stale K slot, on a causal
+        // wave's last tile from keys past its diagonal); a wave then issues
+        // only the loads and barriers of the tiles past its diagonal.  The
+        // variant without S(t+1) sits outside the loop: inside it, the two
+        // bodies together spilled.
         auto iter = [&](int t, f32x16 (&s_cur)[KB], f32x16 (&s_nxt)[KB], auto mask_tag) __attribute__((always_inline)) {
             const bool odd = t & 1;
             dma(t + 2 < n_tiles ? t + 2 : -1, odd ? KS1 : KS0,
@@ -849,9 +853,10 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
             tile_barrier();
         };
         // Two loops, one per masking mode of the next tile, each running two
-        // tiles per trip (score sets A and B alternate).  The second loop
-        // starts with the current scores in set A.
-        const int split = max(0, min(first_masked - 1, n_tiles));
+        // tiles per trip (score sets A and B alternate).  The second loop, and
+        // the last active tile, start with the current scores in set A.
+        const int t_last = CAUSAL ? min(n_tiles - 1, (q_wave0 + 31 + diag) / BN) : n_tiles - 1;
+        const int split = max(0, min(first_masked - 1, t_last));
         auto run = [&](int t0, int t1, auto mask_tag) __attribute__((always_inline)) {
             for (int t = t0; t < t1; t += 2) {
                 iter(t, sA, sB, mask_tag);
@@ -863,7 +868,27 @@ __global__ __launch_bounds__(NW * 64, (fwd_waves_per_eu<D, BN, NW, PIPE>())) voi
 #pragma unroll
             for (int kb = 0; kb < KB; ++kb) sA[kb] = sB[kb];
         }
-        run(split, n_tiles, std::true_type{});
+        run(split, t_last, std::true_type{});
+        if ((t_last - split) & 1) {
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb) sA[kb] = sB[kb];
+        }
+        {
+            const int t = t_last;
+            const bool odd = t & 1;
+            dma(t + 2 < n_tiles ? t + 2 : -1, odd ? KS1 : KS0, t + 1 < n_tiles ? t + 1 : -1,
+                odd ? VS0 : VS1);
+            const float m_ref = update_ref(mx_next);
+            fused_tile(odd ? kslot0 : kslot1, odd ? vslot1 : vslot0, sA, sB, pb, t, m_ref,
+                       std::false_type{}, std::true_type{});
+            tile_barrier();
+        }
+        for (int t = t_last + 1; t < n_tiles; ++t) {
+            const bool odd = t & 1;
+            dma(t + 2 < n_tiles ? t + 2 : -1, odd ? KS1 : KS0, t + 1 < n_tiles ? t + 1 : -1,
+                odd ? VS0 : VS1);
+            tile_barrier();
+        }
     }
 
     // The next q-tile's Q is fetched before this one's output is stored, so
