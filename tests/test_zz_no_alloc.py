@@ -60,9 +60,10 @@ def _case(pa, B, Hq, Hkv, Skv, d, n_splits, seed):
 
 @pytest.mark.parametrize("pair", [
     # (larger call, then a smaller one) -- B, Hq, Hkv, Skv, d, n_splits
-    ((16, 32, 32, 2048, 128, 0), (2, 4, 4, 300, 128, 3)),      # VALU kernel, planner's splits
+    ((16, 32, 32, 2048, 128, 4), (2, 4, 4, 300, 128, 3)),      # VALU kernel, partials in the scratch
     ((4, 32, 4, 5000, 128, 16), (1, 8, 1, 777, 128, 5)),       # grouped heads, matrix cores
-    ((3, 8, 8, 4099, 64, 64), (1, 2, 2, 17, 64, 0)),           # d = 64, many splits
+    ((3, 8, 8, 4099, 64, 64), (1, 2, 2, 17, 64, 0)),           # d = 64, many splits; then one
+                                                               # split, which bypasses the scratch
 ], ids=["mha", "gqa_mfma", "d64"])
 def test_noalloc_matches_allocating_decode(pa, pair):
     for i, (B, Hq, Hkv, Skv, d, n) in enumerate(pair):
